@@ -1,0 +1,227 @@
+"""Plain CPU oracle of the HiLoRe hot path (test infrastructure only).
+
+Only the test suite, ``__graft_entry__.smoke()`` and the CPU-baseline leg of
+``bench.py`` import this package.  The GPU product path never does: the oracle
+and the HIP library share no code, header or table.
+
+The arithmetic lives in ``oracle.c`` (plain single-threaded C, fp32 where the
+GPU must match bit for bit, fp64 for every tolerance-checked "truth" value);
+this module only marshals numpy arrays through ctypes.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB = os.path.join(_HERE, "liboracle.so")
+
+INT8 = 0
+E4M3FN = 1
+
+GCC_FLAGS = ["-O2", "-std=c11", "-Wall", "-Wextra", "-ffp-contract=off", "-fno-fast-math",
+             "-fPIC", "-shared"]
+
+
+def build(force: bool = True) -> str:
+    """Compile liboracle.so with gcc (plain C, no FMA contraction)."""
+    if force or not os.path.exists(_LIB):
+        tmp = _LIB + ".tmp"
+        subprocess.run(["gcc", *GCC_FLAGS, _SRC, "-o", tmp, "-lm"], check=True)
+        os.replace(tmp, _LIB)
+    return _LIB
+
+
+_lib = None
+
+
+def lib() -> ctypes.CDLL:
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB):
+            build(force=True)
+        L = ctypes.CDLL(_LIB)
+        P = ctypes.c_void_p
+        i64 = ctypes.c_int64
+        i32 = ctypes.c_int
+        f32 = ctypes.c_float
+        f64 = ctypes.c_double
+        sig = {
+            "orc_bf16_to_f32": (f32, [ctypes.c_uint16]),
+            "orc_bf16_rne": (ctypes.c_uint16, [f32]),
+            "orc_e4m3fn_rne": (ctypes.c_uint8, [f32]),
+            "orc_e4m3fn_decode": (f64, [ctypes.c_uint8]),
+            "orc_code_value": (f32, [i32, ctypes.c_uint8]),
+            "orc_bf16_rne_array": (None, [P, i64, P]),
+            "orc_e4m3fn_rne_array": (None, [P, i64, P]),
+            "orc_grpo_advantages": (None, [P, i32, i32, f32, P]),
+            "orc_grpo_coeffs": (None, [P, P, P, P, P, i32, i32, i32, f32, f32, f64, f64,
+                                       P, P, P, P]),
+            "orc_grpo_loss": (f64, [P, P, P, P, P, i32, i32, f64, f64, f64]),
+            "orc_quantize": (None, [P, i64, i64, i64, i32, i32, P, P]),
+            "orc_dequantize": (None, [P, P, i64, i64, i32, i32, P]),
+            "orc_row_stats": (None, [P, i64, P, i64, i64, P, P]),
+            "orc_unit_exposure_risk": (None, [P, P, i64, P, P, i64, f64, f64, P, P, P]),
+            "orc_wgrad": (None, [P, P, i32, i32, P, i64, i64, i64, i64, i64, i64, i64, i32, P]),
+            "orc_wgrad_entries": (None, [P, P, i32, i32, P, i64, i64, i64, P, P, i64, i32, P]),
+        }
+        for name, (res, args) in sig.items():
+            fn = getattr(L, name)
+            fn.restype = res
+            fn.argtypes = args
+        _lib = L
+    return _lib
+
+
+def _ptr(a):
+    if a is None:
+        return None
+    assert a.flags["C_CONTIGUOUS"], "oracle inputs must be C-contiguous"
+    return a.ctypes.data_as(ctypes.c_void_p)
+
+
+def _c(a, dtype):
+    return None if a is None else np.ascontiguousarray(a, dtype=dtype)
+
+
+# ---------------------------------------------------------------- formats --
+def bf16_to_f32(h):
+    return (np.asarray(h, dtype=np.uint16).astype(np.uint32) << 16).view(np.float32)
+
+
+def bf16_rne(v):
+    v = _c(v, np.float32).ravel()
+    out = np.empty(v.size, dtype=np.uint16)
+    lib().orc_bf16_rne_array(_ptr(v), v.size, _ptr(out))
+    return out
+
+
+def e4m3fn_rne(v):
+    v = _c(v, np.float32).ravel()
+    out = np.empty(v.size, dtype=np.uint8)
+    lib().orc_e4m3fn_rne_array(_ptr(v), v.size, _ptr(out))
+    return out
+
+
+def e4m3fn_decode(c: int) -> float:
+    return lib().orc_e4m3fn_decode(int(c))
+
+
+def code_value(code: int, c: int) -> float:
+    return lib().orc_code_value(int(code), int(c))
+
+
+# ------------------------------------------------------------------- GRPO --
+def grpo_advantages(rewards, P, G, adv_eps=1e-6):
+    r = _c(rewards, np.float32)
+    adv = np.empty(P * G, dtype=np.float32)
+    lib().orc_grpo_advantages(_ptr(r), P, G, adv_eps, _ptr(adv))
+    return adv
+
+
+def grpo_coeffs(rewards, logp_new, logp_old, logp_ref, mask, P, G, T, clip_eps=0.2,
+                adv_eps=1e-6, beta=0.0, n_norm=0.0):
+    """Returns (adv f32[R], ratio f64[R*T], flags u8[R*T], coeff f64[R*T])."""
+    n = P * G * T
+    r = _c(rewards, np.float32)
+    ln, lo = _c(logp_new, np.float32), _c(logp_old, np.float32)
+    lr = _c(logp_ref, np.float32)
+    m = _c(mask, np.uint8)
+    adv = np.empty(P * G, dtype=np.float32)
+    ratio = np.empty(n, dtype=np.float64)
+    flags = np.empty(n, dtype=np.uint8)
+    coeff = np.empty(n, dtype=np.float64)
+    lib().orc_grpo_coeffs(_ptr(r), _ptr(ln), _ptr(lo), _ptr(lr), _ptr(m), P, G, T, clip_eps,
+                          adv_eps, float(beta), float(n_norm), _ptr(adv), _ptr(ratio),
+                          _ptr(flags), _ptr(coeff))
+    return adv, ratio, flags, coeff
+
+
+def grpo_loss(adv, logp_new_f64, logp_old, logp_ref, mask, R, T, clip_eps=0.2, beta=0.0,
+              n_norm=0.0):
+    a = _c(adv, np.float32)
+    ln = _c(logp_new_f64, np.float64)
+    lo = _c(logp_old, np.float32)
+    lr = _c(logp_ref, np.float32)
+    m = _c(mask, np.uint8)
+    return lib().orc_grpo_loss(_ptr(a), _ptr(ln), _ptr(lo), _ptr(lr), _ptr(m), R, T,
+                               float(clip_eps), float(beta), float(n_norm))
+
+
+# ------------------------------------------------------------------ codec --
+def quantize(x_u16, code, block, cols=None):
+    """x_u16: uint16 [rows, ld] bf16 bits (ld = row stride); quantises the first
+    ``cols`` columns of every row (all of them by default)."""
+    x = _c(x_u16, np.uint16)
+    rows, ld = x.shape
+    cols = ld if cols is None else cols
+    codes = np.empty((rows, cols), dtype=np.uint8)
+    scales = np.empty((rows, cols // block), dtype=np.float32)
+    lib().orc_quantize(_ptr(x), rows, cols, ld, code, block, _ptr(codes), _ptr(scales))
+    return codes, scales
+
+
+def dequantize(codes, scales, code, block):
+    c = _c(codes, np.uint8)
+    s = _c(scales, np.float32)
+    rows, cols = c.shape
+    xh = np.empty((rows, cols), dtype=np.uint16)
+    lib().orc_dequantize(_ptr(c), _ptr(s), rows, cols, code, block, _ptr(xh))
+    return xh
+
+
+def row_stats(x_u16, xhat_u16):
+    x = _c(x_u16, np.uint16)
+    xh = _c(xhat_u16, np.uint16)
+    rows, cols = xh.shape
+    ss_x = np.empty(rows, dtype=np.float64)
+    ss_e = np.empty(rows, dtype=np.float64)
+    lib().orc_row_stats(_ptr(x), x.shape[1], _ptr(xh), rows, cols, _ptr(ss_x), _ptr(ss_e))
+    return ss_x, ss_e
+
+
+def unit_exposure_risk(coeff, mask, ss_x, ss_err, d_u, eps_alpha=1e-8, eps_rel=1e-8):
+    w = _c(coeff, np.float64)
+    m = _c(mask, np.uint8)
+    sx = _c(ss_x, np.float64)
+    se = _c(ss_err, np.float64)
+    e = ctypes.c_double()
+    k = ctypes.c_double()
+    rel = ctypes.c_double()
+    lib().orc_unit_exposure_risk(_ptr(w), _ptr(m), sx.size, _ptr(sx), _ptr(se), int(d_u),
+                                 float(eps_alpha), float(eps_rel), ctypes.byref(e),
+                                 ctypes.byref(k), ctypes.byref(rel))
+    return e.value, k.value, rel.value
+
+
+# ------------------------------------------------------------------ wgrad --
+def wgrad(codes, scales, code, block, dy_u16, i0=0, i1=None, j0=0, j1=None, variant=0):
+    c = _c(codes, np.uint8)
+    s = _c(scales, np.float32)
+    d = _c(dy_u16, np.uint16)
+    K, M = c.shape
+    N = d.shape[1]
+    i1 = M if i1 is None else i1
+    j1 = N if j1 is None else j1
+    out = np.empty((i1 - i0, j1 - j0), dtype=np.float64)
+    lib().orc_wgrad(_ptr(c), _ptr(s), code, block, _ptr(d), K, M, N, i0, i1, j0, j1, variant,
+                    _ptr(out))
+    return out
+
+
+def wgrad_entries(codes, scales, code, block, dy_u16, ii, jj, variant=0, K=None):
+    c = _c(codes, np.uint8)
+    s = _c(scales, np.float32)
+    d = _c(dy_u16, np.uint16)
+    Kc, M = c.shape
+    N = d.shape[1]
+    ii = _c(ii, np.int64)
+    jj = _c(jj, np.int64)
+    out = np.empty(ii.size, dtype=np.float64)
+    lib().orc_wgrad_entries(_ptr(c), _ptr(s), code, block, _ptr(d), Kc if K is None else K, M,
+                            N, _ptr(ii), _ptr(jj), ii.size, variant, _ptr(out))
+    return out

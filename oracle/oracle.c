@@ -1,0 +1,399 @@
+/*
+ * oracle.c -- plain, slow, single-threaded CPU reference of the HiLoRe hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY: loaded by the tests, the smoke check and the
+ * benchmark's CPU-baseline leg; never by the GPU product path.  It shares no
+ * code, header, table or constant generator with the GPU library.
+ *
+ * Everything here is written for a reader holding the paper: each routine is
+ * the definition the paper gives (or the reading stated next to it), with no
+ * blocking, fusion or reordering beyond what that definition states.
+ */
+#include "oracle.h"
+
+#include <math.h>
+#include <stdlib.h>
+#include <string.h>
+
+static float f32_from_bits(uint32_t u) { float f; memcpy(&f, &u, sizeof f); return f; }
+static uint32_t bits_from_f32(float f) { uint32_t u; memcpy(&u, &f, sizeof u); return u; }
+
+/* ======================================================================= */
+/* Number formats                                                          */
+/* ======================================================================= */
+
+/* bf16 is the upper half of a binary32 word: widening is exact. */
+float orc_bf16_to_f32(uint16_t h) { return f32_from_bits((uint32_t)h << 16); }
+
+/* fp32 -> bf16 with round-to-nearest, ties to even, written as the rule
+ * itself: find the two bf16 neighbours of v, keep the nearer one, and on a
+ * tie keep the one whose last mantissa bit is 0.  Overflow past the largest
+ * bf16 goes to infinity exactly as IEEE rounding with an unbounded exponent
+ * would (the would-be next value is 2^128).  NaN inputs are out of contract. */
+uint16_t orc_bf16_rne(float v) {
+  uint32_t u = bits_from_f32(v);
+  if ((u & 0x7F800000u) == 0x7F800000u) return (uint16_t)(u >> 16); /* +-inf */
+  uint32_t down = u & 0xFFFF0000u;              /* toward zero, same sign */
+  uint32_t up = down + 0x10000u;                /* next magnitude */
+  double mag = fabs((double)v);
+  double lo = fabs((double)f32_from_bits(down));
+  double hi = ((up & 0x7F800000u) == 0x7F800000u) ? ldexp(1.0, 128)
+                                                  : fabs((double)f32_from_bits(up));
+  double dl = mag - lo, dh = hi - mag;          /* exact in double */
+  if (dl < dh) return (uint16_t)(down >> 16);
+  if (dh < dl) return (uint16_t)(up >> 16);
+  return (uint16_t)((((down >> 16) & 1u) == 0u) ? (down >> 16) : (up >> 16));
+}
+
+/* Exact value of an OCP E4M3FN code: 1 sign bit, 4 exponent bits (bias 7),
+ * 3 mantissa bits; exponent field 0 holds subnormals m * 2^-9; S.1111.111 is
+ * NaN and there are no infinities.  This is the format torch.float8_e4m3fn
+ * names (App. B.1, Eq. fp8-roundtrip). */
+double orc_e4m3fn_decode(uint8_t c) {
+  int s = (c >> 7) & 1, e = (c >> 3) & 15, m = c & 7;
+  if (e == 15 && m == 7) return NAN;
+  double mag = (e == 0) ? ldexp((double)m, -9) : ldexp(1.0 + m / 8.0, e - 7);
+  return s ? -mag : mag;
+}
+
+/* fp32 -> E4M3FN, round to nearest with ties to even on the E4M3FN grid,
+ * saturating at +-448, keeping the sign of zero.  Done by exact arithmetic in
+ * double: the grid spacing in the binade of |v| is 2^(max(e,-6)-3); round
+ * |v| / spacing to the nearest integer (ties to the even integer), multiply
+ * back, then encode the resulting grid value. */
+uint8_t orc_e4m3fn_rne(float v) {
+  uint8_t sign = (bits_from_f32(v) >> 31) ? 0x80 : 0x00;
+  double a = fabs((double)v);
+  if (a == 0.0) return sign;
+  int ex;
+  frexp(a, &ex);                                /* a = f * 2^ex, f in [0.5,1) */
+  int e = ex - 1;                               /* a in [2^e, 2^(e+1)) */
+  int qe = (e < -6 ? -6 : e) - 3;               /* spacing exponent */
+  double n = ldexp(a, -qe);                     /* exact */
+  double fl = floor(n), frac = n - fl;
+  double k;
+  if (frac > 0.5) k = fl + 1.0;
+  else if (frac < 0.5) k = fl;
+  else k = (fmod(fl, 2.0) == 0.0) ? fl : fl + 1.0;
+  double g = ldexp(k, qe);                      /* rounded grid value */
+  if (g > 448.0) g = 448.0;                     /* saturate */
+  uint8_t code;
+  if (g < ldexp(1.0, -6)) {
+    code = (uint8_t)ldexp(g, 9);                /* subnormal: g = m * 2^-9, m in 0..7 */
+  } else {
+    int gx;
+    frexp(g, &gx);
+    int ge = gx - 1;                            /* g in [2^ge, 2^(ge+1)) */
+    int mant = (int)ldexp(g, 3 - ge) - 8;       /* 3-bit mantissa */
+    code = (uint8_t)(((ge + 7) << 3) | mant);
+  }
+  return (uint8_t)(sign | code);
+}
+
+void orc_bf16_rne_array(const float *v, int64_t n, uint16_t *out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_bf16_rne(v[i]);
+}
+
+void orc_e4m3fn_rne_array(const float *v, int64_t n, uint8_t *out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_e4m3fn_rne(v[i]);
+}
+
+float orc_code_value(int code, uint8_t c) {
+  if (code == ORC_INT8) return (float)(int8_t)c;
+  return (float)orc_e4m3fn_decode(c);
+}
+
+/* ======================================================================= */
+/* GRPO                                                                    */
+/* ======================================================================= */
+
+/* Pairwise sum: the values padded with +0 to a power-of-two count, then
+ * summed as (first half) + (second half), recursively, in fp32. */
+static float pairsum_rec(const float *v, int lo, int len, int n) {
+  if (len == 1) return lo < n ? v[lo] : 0.0f;
+  int h = len / 2;
+  return pairsum_rec(v, lo, h, n) + pairsum_rec(v, lo + h, h, n);
+}
+static float pairsum(const float *v, int n) {
+  int p2 = 1;
+  while (p2 < n) p2 *= 2;
+  return pairsum_rec(v, 0, p2, n);
+}
+
+/* Group-relative advantages (Sec. 3.1; App. D.1.1 "GRPO and optimization"):
+ * for each prompt, over its G responses, A = (R - mean) / (population std +
+ * adv_eps); a group whose rewards are all equal gets A = 0.  fp32, with the
+ * pairwise sums above so that the GPU can reproduce every bit. */
+void orc_grpo_advantages(const float *rewards, int P, int G, float adv_eps, float *adv) {
+  float *d = (float *)malloc(sizeof(float) * (size_t)(G > 0 ? G : 1));
+  float *sq = (float *)malloc(sizeof(float) * (size_t)(G > 0 ? G : 1));
+  for (int i = 0; i < P; ++i) {
+    const float *r = rewards + (size_t)i * G;
+    float mu = pairsum(r, G) / (float)G;
+    for (int j = 0; j < G; ++j) { d[j] = r[j] - mu; sq[j] = d[j] * d[j]; }
+    float sigma = sqrtf(pairsum(sq, G) / (float)G);
+    for (int j = 0; j < G; ++j) adv[(size_t)i * G + j] = d[j] / (sigma + adv_eps);
+  }
+  free(d);
+  free(sq);
+}
+
+static double count_valid(const uint8_t *mask, int64_t n) {
+  if (!mask) return (double)n;
+  int64_t c = 0;
+  for (int64_t i = 0; i < n; ++i) c += mask[i] != 0;
+  return (double)c;
+}
+
+/* Per-token quantities of the GRPO update for responses laid out
+ * response-major, T slots each (slot j*T + t is token t of response j):
+ *   ratio  r_t = exp(s_t - s_t^old)                        (Sec. 3.1)
+ *   chi_t  = [(A >= 0 and r <= 1+eps) or (A < 0 and r >= 1-eps)]
+ *                                                          (Eq. update-coefficient)
+ *   flags  bit0 = m and chi (policy term active)
+ *          bit1 = m and A != 0 and not chi (clipped, Eq. diagnostic-clipping)
+ *   coeff  omega_t = dL/ds_t = -(m/N) chi r A + beta (m/N) [1 - exp(s_ref - s)]
+ *          (Eq. update-coefficient; K3 derivative in the proof of Prop. 1)
+ * Readings: chi is decided in log-ratio space, delta = s - s_old in fp32
+ * against the fp32 thresholds log1p(+-eps) (the paper leaves the boundary to
+ * the implementation); N is n_norm when positive (the whole rollout batch,
+ * App. D.1.1), else the count of valid slots in this call; N = 0 gives
+ * omega = 0.  Masked slots (mask byte 0) have omega = 0 and flags = 0.
+ * adv/flags are the fp32/integer values the GPU must match exactly; ratio and
+ * coeff are fp64 truth. */
+void orc_grpo_coeffs(const float *rewards, const float *logp_new, const float *logp_old,
+                     const float *logp_ref, const uint8_t *mask, int P, int G, int T,
+                     float clip_eps, float adv_eps, double beta, double n_norm,
+                     float *adv, double *ratio, uint8_t *flags, double *coeff) {
+  const int64_t R = (int64_t)P * G;
+  const int64_t n = R * (int64_t)T;
+  orc_grpo_advantages(rewards, P, G, adv_eps, adv);
+  const float hi = (float)log1p((double)clip_eps);
+  const float lo = (float)log1p(-(double)clip_eps);
+  const double N = n_norm > 0.0 ? n_norm : count_valid(mask, n);
+  for (int64_t j = 0; j < R; ++j) {
+    const float A = adv[j];
+    for (int64_t t = 0; t < T; ++t) {
+      const int64_t i = j * T + t;
+      const int m = mask ? (mask[i] != 0) : 1;
+      const float delta = logp_new[i] - logp_old[i];
+      const int chi = (A >= 0.0f) ? (delta <= hi) : (delta >= lo);
+      flags[i] = (uint8_t)((m && chi ? 1 : 0) | (m && A != 0.0f && !chi ? 2 : 0));
+      const double r = exp((double)logp_new[i] - (double)logp_old[i]);
+      if (ratio) ratio[i] = r;
+      double w = 0.0;
+      if (m && N > 0.0) {
+        const double pol = chi ? r * (double)A : 0.0;
+        const double kl = (beta != 0.0)
+            ? beta * expm1((double)logp_ref[i] - (double)logp_new[i]) : 0.0;
+        w = (-pol - kl) / N;
+      }
+      coeff[i] = w;
+    }
+  }
+}
+
+/* The GRPO objective itself (Sec. 3.1, Eq. grpo-objective, with the K3 KL of
+ * the proof of Prop. 1), in fp64, as a function of the current log-probs, for
+ * finite-difference checks of the coefficients:
+ *   L = -(1/N) sum m min(r A, clip(r, 1-eps, 1+eps) A)
+ *       + beta (1/N) sum m [exp(s_ref - s) - (s_ref - s) - 1].          */
+double orc_grpo_loss(const float *adv, const double *logp_new, const float *logp_old,
+                     const float *logp_ref, const uint8_t *mask, int R, int T,
+                     double clip_eps, double beta, double n_norm) {
+  const int64_t n = (int64_t)R * T;
+  const double N = n_norm > 0.0 ? n_norm : count_valid(mask, n);
+  if (N <= 0.0) return 0.0;
+  double L = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    if (mask && !mask[i]) continue;
+    const double A = (double)adv[i / T];
+    const double r = exp(logp_new[i] - (double)logp_old[i]);
+    double rc = r;
+    if (rc < 1.0 - clip_eps) rc = 1.0 - clip_eps;
+    if (rc > 1.0 + clip_eps) rc = 1.0 + clip_eps;
+    const double a = r * A, b = rc * A;
+    L -= (a < b ? a : b);
+    if (beta != 0.0) {
+      const double x = (double)logp_ref[i] - logp_new[i];
+      L += beta * (exp(x) - x - 1.0);
+    }
+  }
+  return L / N;
+}
+
+/* ======================================================================= */
+/* Blockwise absmax codec                                                  */
+/* ======================================================================= */
+
+/* The paper's low-precision action stores an FP8 E4M3FN copy of a bf16
+ * activation and casts it back for backward (App. B.1, Eq. fp8-roundtrip).
+ * This build uses the scaled reading of that codec: every run of `block`
+ * consecutive elements of a row gets one fp32 scale.  Step by step, with
+ * Q = 127 (int8) or 448 (E4M3FN):
+ *   amax = max |x_j| over the block (exact: bf16 widens to fp32 exactly);
+ *   if amax < 2^-64 (zero or negligible block): scale = 0, codes = 0;
+ *   else  s = amax / Q  and  r = Q / amax   (IEEE fp32 divisions),
+ *         v_j = x_j * r                      (fp32 multiply),
+ *         int8:   q_j = clamp(nearest-even integer of v_j, -127, 127),
+ *         E4M3FN: q_j = orc_e4m3fn_rne(v_j). */
+void orc_quantize(const uint16_t *x, int64_t rows, int64_t cols, int64_t ld, int code,
+                  int block, uint8_t *codes, float *scales) {
+  const float Q = (code == ORC_INT8) ? 127.0f : 448.0f;
+  const float tiny = ldexpf(1.0f, -64);
+  const int64_t nb = cols / block;
+  for (int64_t row = 0; row < rows; ++row) {
+    for (int64_t b = 0; b < nb; ++b) {
+      const uint16_t *xb = x + row * ld + b * block;
+      uint8_t *cb = codes + row * cols + b * block;
+      float amax = 0.0f;
+      for (int j = 0; j < block; ++j) {
+        const float a = fabsf(orc_bf16_to_f32(xb[j]));
+        if (a > amax) amax = a;
+      }
+      if (!(amax >= tiny)) {
+        scales[row * nb + b] = 0.0f;
+        for (int j = 0; j < block; ++j) cb[j] = 0;
+        continue;
+      }
+      const float s = amax / Q;
+      const float r = Q / amax;
+      scales[row * nb + b] = s;
+      for (int j = 0; j < block; ++j) {
+        const float v = orc_bf16_to_f32(xb[j]) * r;
+        if (code == ORC_INT8) {
+          float q = nearbyintf(v);              /* default mode: nearest, ties even */
+          if (q > 127.0f) q = 127.0f;
+          if (q < -127.0f) q = -127.0f;
+          cb[j] = (uint8_t)(int8_t)(int)q;
+        } else {
+          cb[j] = orc_e4m3fn_rne(v);
+        }
+      }
+    }
+  }
+}
+
+/* Reconstruction (App. B.1, Eq. fp8-roundtrip, the cast back to BF16):
+ * xhat = bf16_rne( value(q) * s ), the product an fp32 multiply. */
+void orc_dequantize(const uint8_t *codes, const float *scales, int64_t rows, int64_t cols,
+                    int code, int block, uint16_t *xhat) {
+  const int64_t nb = cols / block;
+  for (int64_t row = 0; row < rows; ++row)
+    for (int64_t c = 0; c < cols; ++c) {
+      const float q = orc_code_value(code, codes[row * cols + c]);
+      const float s = scales[row * nb + c / block];
+      xhat[row * cols + c] = orc_bf16_rne(q * s);
+    }
+}
+
+/* Per-row sums in fp64: ss_x = sum x^2 (for the token RMS a_t of Eq.
+ * activation-token-weights) and ss_err = sum (xhat - x)^2 (for the
+ * reconstruction error of Eq. app-calibration-error). */
+void orc_row_stats(const uint16_t *x, int64_t ld, const uint16_t *xhat, int64_t rows,
+                   int64_t cols, double *ss_x, double *ss_err) {
+  for (int64_t row = 0; row < rows; ++row) {
+    double sx = 0.0, se = 0.0;
+    for (int64_t c = 0; c < cols; ++c) {
+      const double xv = (double)orc_bf16_to_f32(x[row * ld + c]);
+      const double hv = (double)orc_bf16_to_f32(xhat[row * cols + c]);
+      sx += xv * xv;
+      se += (hv - xv) * (hv - xv);
+    }
+    if (ss_x) ss_x[row] = sx;
+    if (ss_err) ss_err[row] = se;
+  }
+}
+
+/* ======================================================================= */
+/* Exposure and risk of one unit                                           */
+/* ======================================================================= */
+
+/* For one unit of width d_u over the rows (tokens) of a microbatch, with
+ * T = rows whose mask byte is nonzero (all rows if mask is NULL):
+ *   a_t      = sqrt(ss_x_t / d_u)                       (Eq. activation-token-weights)
+ *   alpha_t  = (a_t + eps_a) / (mean_{s in T} a_s + eps_a)
+ *   exposure = sum_{t in T} |omega_t| alpha_t            (Eq. mlp-weighted-exposure)
+ *   risk     = sum_{t in T} |omega_t| sqrt(ss_err_t)     (token-weighted reconstruction
+ *              error, the first-order bound of Thm. 1 for a linear consumer)
+ *   rel_err  = sqrt(sum_t ss_err_t) / (sqrt(sum_t ss_x_t) + eps_rel) over all rows
+ *                                                        (Eq. app-calibration-error)
+ * An empty T gives exposure = risk = 0. */
+void orc_unit_exposure_risk(const double *coeff, const uint8_t *mask, int64_t rows,
+                            const double *ss_x, const double *ss_err, int64_t d_u,
+                            double eps_alpha, double eps_rel,
+                            double *exposure, double *risk, double *rel_err) {
+  double sum_a = 0.0, cnt = 0.0, sx = 0.0, se = 0.0;
+  for (int64_t t = 0; t < rows; ++t) {
+    sx += ss_x[t];
+    se += ss_err[t];
+    if (mask && !mask[t]) continue;
+    sum_a += sqrt(ss_x[t] / (double)d_u);
+    cnt += 1.0;
+  }
+  double e = 0.0, k = 0.0;
+  if (cnt > 0.0) {
+    const double mean_a = sum_a / cnt;
+    for (int64_t t = 0; t < rows; ++t) {
+      if (mask && !mask[t]) continue;
+      const double a = sqrt(ss_x[t] / (double)d_u);
+      const double alpha = (a + eps_alpha) / (mean_a + eps_alpha);
+      e += fabs(coeff[t]) * alpha;
+      k += fabs(coeff[t]) * sqrt(ss_err[t]);
+    }
+  }
+  *exposure = e;
+  *risk = k;
+  *rel_err = sqrt(se) / (sqrt(sx) + eps_rel);
+}
+
+/* ======================================================================= */
+/* Weight gradient on reconstructed activations                            */
+/* ======================================================================= */
+
+static double deq_value(const uint8_t *codes, const float *scales, int code, int block,
+                        int64_t M, int64_t t, int64_t i, int variant) {
+  const uint8_t c = codes[t * M + i];
+  const float s = scales[t * (M / block) + i / block];
+  if (variant == 0) {
+    const double q = (code == ORC_INT8) ? (double)(int8_t)c : orc_e4m3fn_decode(c);
+    return q * (double)s;
+  }
+  return (double)orc_bf16_to_f32(orc_bf16_rne(orc_code_value(code, c) * s));
+}
+
+/* dW[i][j] = sum_t Xtilde[t][i] * dY[t][j] in fp64 (the full-parameter weight
+ * gradient of a linear layer whose saved input was recovered from its
+ * low-precision copy; its relative Frobenius error against this is the
+ * measure of Eq. measured-gradient-error). */
+void orc_wgrad(const uint8_t *codes, const float *scales, int code, int block,
+               const uint16_t *dy, int64_t K, int64_t M, int64_t N,
+               int64_t i0, int64_t i1, int64_t j0, int64_t j1, int variant, double *out) {
+  const int64_t w = j1 - j0;
+  for (int64_t i = 0; i < (i1 - i0) * w; ++i) out[i] = 0.0;
+  double *xcol = (double *)malloc(sizeof(double) * (size_t)(i1 - i0 > 0 ? i1 - i0 : 1));
+  for (int64_t t = 0; t < K; ++t) {
+    for (int64_t i = i0; i < i1; ++i)
+      xcol[i - i0] = deq_value(codes, scales, code, block, M, t, i, variant);
+    for (int64_t i = i0; i < i1; ++i) {
+      const double xv = xcol[i - i0];
+      double *o = out + (i - i0) * w;
+      const uint16_t *dr = dy + t * N;
+      for (int64_t j = j0; j < j1; ++j) o[j - j0] += xv * (double)orc_bf16_to_f32(dr[j]);
+    }
+  }
+  free(xcol);
+}
+
+void orc_wgrad_entries(const uint8_t *codes, const float *scales, int code, int block,
+                       const uint16_t *dy, int64_t K, int64_t M, int64_t N,
+                       const int64_t *ii, const int64_t *jj, int64_t n, int variant,
+                       double *out) {
+  for (int64_t e = 0; e < n; ++e) {
+    double acc = 0.0;
+    for (int64_t t = 0; t < K; ++t)
+      acc += deq_value(codes, scales, code, block, M, t, ii[e], variant) *
+             (double)orc_bf16_to_f32(dy[t * N + jj[e]]);
+    out[e] = acc;
+  }
+}

@@ -1,0 +1,90 @@
+/*
+ * oracle.h -- plain, slow, single-threaded CPU reference of the HiLoRe hot path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the test suite, the smoke check and the
+ * CPU-baseline leg of the benchmark load this library.  The GPU product path
+ * (libhilore) never includes, links or calls anything in this directory, and
+ * this directory never includes anything from the product path.
+ *
+ * Paper: "HiLoRe: What to Store, Compress, or Recompute for Efficient GRPO
+ * Training".  Each function cites the passage it follows.
+ *
+ * Precision rules:
+ *   - values the GPU must reproduce bit for bit (advantages, clip flags,
+ *     quantisation codes, block scales, dequantised bf16 values) are computed
+ *     in fp32 with the exact operation sequence written out below;
+ *   - every value checked against a tolerance (ratios, loss coefficients, row
+ *     sums, exposure, risk, relative error, weight gradients) is computed in
+ *     fp64 and serves as the "truth".
+ *
+ * Build: gcc -O2 -std=c11 -ffp-contract=off -fno-fast-math (x86-64 SSE, so
+ * every float operation is a single IEEE binary32 operation, rounded to
+ * nearest even, with no fused multiply-add).
+ */
+#ifndef HILORE_ORACLE_H
+#define HILORE_ORACLE_H
+
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+enum { ORC_INT8 = 0, ORC_E4M3FN = 1 };
+
+/* ---- number formats --------------------------------------------------- */
+float    orc_bf16_to_f32(uint16_t h);
+uint16_t orc_bf16_rne(float v);            /* fp32 -> bf16, nearest-even, by distances */
+uint8_t  orc_e4m3fn_rne(float v);          /* fp32 -> OCP E4M3FN, nearest-even, saturating */
+double   orc_e4m3fn_decode(uint8_t c);     /* exact value of an E4M3FN code (NaN for 0x7f/0xff) */
+float    orc_code_value(int code, uint8_t c); /* exact fp32 value of an int8 / E4M3FN code */
+/* element-wise array forms of the two roundings, for exhaustive checks */
+void     orc_bf16_rne_array(const float *v, int64_t n, uint16_t *out);
+void     orc_e4m3fn_rne_array(const float *v, int64_t n, uint8_t *out);
+
+/* ---- GRPO (Sec. 3.1 Eq. grpo-objective; Sec. 3.2 Eq. update-coefficient) */
+void orc_grpo_advantages(const float *rewards, int P, int G, float adv_eps, float *adv);
+
+void orc_grpo_coeffs(const float *rewards, const float *logp_new, const float *logp_old,
+                     const float *logp_ref, const uint8_t *mask, int P, int G, int T,
+                     float clip_eps, float adv_eps, double beta, double n_norm,
+                     float *adv, double *ratio, uint8_t *flags, double *coeff);
+
+double orc_grpo_loss(const float *adv, const double *logp_new, const float *logp_old,
+                     const float *logp_ref, const uint8_t *mask, int R, int T,
+                     double clip_eps, double beta, double n_norm);
+
+/* ---- blockwise absmax codec (App. B.1 Eq. fp8-roundtrip, scaled reading) */
+void orc_quantize(const uint16_t *x, int64_t rows, int64_t cols, int64_t ld, int code,
+                  int block, uint8_t *codes, float *scales);
+void orc_dequantize(const uint8_t *codes, const float *scales, int64_t rows, int64_t cols,
+                    int code, int block, uint16_t *xhat);
+void orc_row_stats(const uint16_t *x, int64_t ld, const uint16_t *xhat, int64_t rows,
+                   int64_t cols, double *ss_x, double *ss_err);
+
+/* ---- exposure / risk (App. B.1 Eqs. activation-token-weights,
+ *      mlp-weighted-exposure, app-calibration-error; Sec. 3.4) */
+void orc_unit_exposure_risk(const double *coeff, const uint8_t *mask, int64_t rows,
+                            const double *ss_x, const double *ss_err, int64_t d_u,
+                            double eps_alpha, double eps_rel,
+                            double *exposure, double *risk, double *rel_err);
+
+/* ---- weight gradient on reconstructed activations: dW = deq(X)^T dY ----
+ * variant 0: deq = code value * scale in fp64 (unrounded);
+ * variant 1: deq = the bf16 value orc_dequantize produces.
+ * Computes dW[i][j] for i in [i0,i1), j in [j0,j1) into out[(i-i0)*(j1-j0)+(j-j0)]. */
+void orc_wgrad(const uint8_t *codes, const float *scales, int code, int block,
+               const uint16_t *dy, int64_t K, int64_t M, int64_t N,
+               int64_t i0, int64_t i1, int64_t j0, int64_t j1, int variant, double *out);
+
+/* dW entries at arbitrary (i, j) pairs (for sampled checks at full size). */
+void orc_wgrad_entries(const uint8_t *codes, const float *scales, int code, int block,
+                       const uint16_t *dy, int64_t K, int64_t M, int64_t N,
+                       const int64_t *ii, const int64_t *jj, int64_t n, int variant,
+                       double *out);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif
