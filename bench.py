@@ -1,0 +1,290 @@
+"""Benchmark of the HiLoRe hot path on one MI355X.
+
+One step = one pass of the whole hot path over one microbatch of the
+Qwen2-7B-width layer workload (8 responses x 2048 tokens = 16384 rows), in the
+order of Algorithm 1:
+  1. hilore_grpo_coeffs        GRPO coefficients for the 16384 token slots
+  2. hilore_compress           hidden 16384x3584 + MLP 16384x18944 -> fp8-e4m3 1x128,
+                               with per-row sums (one batched call)
+  3. hilore_unit_exposure_risk exposure / risk / relative error of both units
+  4. hilore_decompress         both units back to bf16 (one batched call)
+  5. hilore_dequant_wgrad      dW 4096x4096 = deq(X)^T dY, X fp8-e4m3 1x128
+                               16384x4096, dY bf16 16384x4096 (fp32 accumulate)
+Inputs are synthetic (seeded, drawn on the device) and resident in HBM before
+the timed region; four buffer sets are rotated so that consecutive steps do
+not hit the 256 MB infinity cache with the previous step's data.
+
+Prints ONE JSON line.  `value` is compress+decompress throughput in GB/s of
+algorithmic bytes (the first figure of the metric); the wgrad TFLOP/s and the
+coefficient tokens/s ride along, each with its own roofline.
+"""
+from __future__ import annotations
+
+import argparse
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+sys.path.insert(0, ROOT)
+
+METRIC = "compress+decompress GB/s (% HBM peak); fused dequant-wgrad TFLOP/s; coeff tok/s"
+HBM_PEAK_GBS = 8000.0
+BF16_PEAK_TFLOPS = 2500.0
+N_SETS = 4
+
+
+def parse():
+    p = argparse.ArgumentParser(description=__doc__.split("\n\n")[0])
+    p.add_argument("--gpus", type=int, default=1)
+    p.add_argument("--steps", type=int, default=20)
+    p.add_argument("--warmup", type=int, default=5)
+    p.add_argument("--no-cpu-baseline", action="store_true")
+    p.add_argument("--cpu-rows", type=int, default=1024,
+                   help="MLP rows (and 4x as many hidden rows) in the oracle's timed sample")
+    return p.parse_args()
+
+
+def codec_bytes(rows, cols, block, stats):
+    """Algorithmic HBM bytes of one compress and one decompress of a unit:
+    read bf16 x, write codes + scales (+ two fp32 row sums); read codes +
+    scales, write bf16 xhat."""
+    n = rows * cols
+    scales = 4 * n // block
+    comp = 2 * n + n + scales + (8 * rows if stats else 0)
+    decomp = n + scales + 2 * n
+    return comp, decomp
+
+
+def main():
+    args = parse()
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
+              "(the hot path shards without communication except one dW reduce-scatter, "
+              "which this build does not implement)", file=sys.stderr)
+        return 2
+
+    import numpy as np
+    import torch
+
+    from paper_2609_33570_amd import hilore as hl
+    from paper_2609_33570_amd import workloads as wl
+
+    hl.load()
+    if not torch.cuda.is_available():
+        print("no GPU visible", file=sys.stderr)
+        return 1
+    torch.cuda.set_device(0)
+
+    w = wl.QWEN2_7B_LAYER
+    ww = wl.WGRAD_4096
+    code, block = hl.HILORE_CODE_FP8_E4M3FN, 128
+    K, M, N = ww.wgrad
+    R = w.P * w.G
+    rows = R * w.T
+    b = wl.grpo_batch(w.P, w.G, w.T, seed=w.seed)
+
+    def progress(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    # ---------------------------------------------------------------- setup --
+    progress("drawing inputs on the device")
+    sets = []
+    for s in range(N_SETS):
+        st = {}
+        st["grpo_host"] = b
+        st["rewards"], st["lp_new"], st["lp_old"] = (torch.from_numpy(a).cuda() for a in
+                                                     (b.rewards, b.logp_new, b.logp_old))
+        st["adv"] = torch.empty(R, dtype=torch.float32, device="cuda")
+        st["flags"] = torch.empty(rows, dtype=torch.uint8, device="cuda")
+        st["coeff"] = torch.empty(rows, dtype=torch.float32, device="cuda")
+        st["ratio"] = torch.empty(rows, dtype=torch.float32, device="cuda")
+        units_c, units_d, keep = [], [], []
+        for i, u in enumerate(w.units):
+            x = wl.activation_device(u.rows, u.cols, w.seed * 10 + i + 1000 * s,
+                                     outliers=w.outliers)
+            codes = torch.empty((u.rows, u.cols), dtype=torch.uint8, device="cuda")
+            scales = torch.empty((u.rows, u.cols // block), dtype=torch.float32, device="cuda")
+            xhat = torch.empty((u.rows, u.cols), dtype=torch.bfloat16, device="cuda")
+            ssx = torch.empty(u.rows, dtype=torch.float32, device="cuda")
+            sse = torch.empty(u.rows, dtype=torch.float32, device="cuda")
+            keep.append((x, codes, scales, xhat, ssx, sse))
+            units_c.append(hl.unit_desc(x=x, codes=codes, scales=scales, row_ss_x=ssx,
+                                        row_ss_err=sse))
+            units_d.append(hl.unit_desc(codes=codes, scales=scales, xhat=xhat))
+        st["keep"], st["uc"], st["ud"] = keep, units_c, units_d
+        st["expo"] = torch.empty(len(w.units), dtype=torch.float32, device="cuda")
+        st["risk"] = torch.empty_like(st["expo"])
+        st["rel"] = torch.empty_like(st["expo"])
+        # wgrad operands: X stored as fp8-e4m3 1x128 (encoded here, outside the timed region)
+        xw = wl.activation_device(K, M, ww.seed + 1000 * s)
+        wc = torch.empty((K, M), dtype=torch.uint8, device="cuda")
+        ws = torch.empty((K, M // block), dtype=torch.float32, device="cuda")
+        hl.hilore_compress([hl.unit_desc(x=xw, codes=wc, scales=ws)], code, block)
+        del xw
+        st["wc"], st["ws"] = wc, ws
+        st["dy"] = wl.normal_bf16_device(K, N, ww.seed + 100 + 1000 * s, 0.02)
+        st["dw"] = torch.empty((M, N), dtype=torch.float32, device="cuda")
+        sets.append(st)
+    torch.cuda.synchronize()
+
+    names = ["grpo_coeffs", "compress", "exposure_risk", "decompress", "dequant_wgrad"]
+
+    def step(st, ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record()
+        mark(0)
+        hl.hilore_grpo_coeffs(st["rewards"], st["lp_new"], st["lp_old"], None, None, w.P, w.G,
+                              w.T, 0.2, 1e-6, 0.0, 0.0, st["adv"], st["ratio"], st["flags"],
+                              st["coeff"])
+        mark(1)
+        hl.hilore_compress(st["uc"], code, block)
+        mark(2)
+        hl.hilore_unit_exposure_risk(st["coeff"], None, rows, st["uc"], 1e-8, 1e-8, st["expo"],
+                                     st["risk"], st["rel"])
+        mark(3)
+        hl.hilore_decompress(st["ud"], code, block)
+        mark(4)
+        hl.hilore_dequant_wgrad(st["wc"], st["ws"], code, block, st["dy"], st["dw"], K, M, N,
+                                False)
+        mark(5)
+
+    progress("warm-up")
+    for i in range(args.warmup):
+        step(sets[i % N_SETS])
+    torch.cuda.synchronize()
+    progress(f"timing {args.steps} steps")
+
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(6)] for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t0 = time.perf_counter()
+    for i in range(args.steps):
+        step(sets[i % N_SETS], events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+
+    per = {n: [] for n in names}
+    for ev in events:
+        for k, n in enumerate(names):
+            per[n].append(ev[k].elapsed_time(ev[k + 1]))
+    avg = {n: float(np.mean(v)) for n, v in per.items()}  # ms
+
+    comp_b = decomp_b = 0
+    for u in w.units:
+        c, d = codec_bytes(u.rows, u.cols, block, stats=True)
+        comp_b += c
+        decomp_b += d
+    codec_gbs = (comp_b + decomp_b) / ((avg["compress"] + avg["decompress"]) * 1e-3) / 1e9
+    wflops = 2.0 * K * M * N
+    wgrad_tflops = wflops / (avg["dequant_wgrad"] * 1e-3) / 1e12
+    coeff_tok_s = rows / (avg["grpo_coeffs"] * 1e-3)
+    grpo_bytes = rows * (4 + 4 + 4 + 4 + 1) + R * 8
+    risk_bytes = rows * (4 + 4) * len(w.units) + rows * 4
+
+    def roof(name, achieved, peak, unit, bound, per_unit):
+        return {"kernel": name, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
+                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                "algorithmic": per_unit}
+
+    roofs = {
+        "compress": roof("compress", comp_b / (avg["compress"] * 1e-3) / 1e9, HBM_PEAK_GBS,
+                         "GB/s", "hbm", f"{comp_b} B per launch (2 units)"),
+        "decompress": roof("decompress", decomp_b / (avg["decompress"] * 1e-3) / 1e9,
+                           HBM_PEAK_GBS, "GB/s", "hbm", f"{decomp_b} B per launch (2 units)"),
+        "dequant_wgrad": roof("dequant_wgrad", wgrad_tflops, BF16_PEAK_TFLOPS, "TFLOP/s", "mfma",
+                              f"{wflops:.0f} FLOP per launch"),
+        "grpo_coeffs": roof("grpo_coeffs", grpo_bytes / (avg["grpo_coeffs"] * 1e-3) / 1e9,
+                            HBM_PEAK_GBS, "GB/s", "hbm", f"{grpo_bytes} B per launch"),
+        "exposure_risk": roof("exposure_risk", risk_bytes / (avg["exposure_risk"] * 1e-3) / 1e9,
+                              HBM_PEAK_GBS, "GB/s", "hbm", f"{risk_bytes} B per launch"),
+    }
+    dominant = max(names, key=lambda n: avg[n])
+
+    out = {
+        "metric": METRIC,
+        "value": round(codec_gbs, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(wall / args.steps * 1e3, 4),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "bf16",
+        "data": "synthetic",
+        "config": {"workload": "qwen2_7b_layer+wgrad_4096",
+                   "tokens": rows, "responses": R, "group": w.G,
+                   "units": [[u.rows, u.cols] for u in w.units], "code": "fp8-e4m3fn",
+                   "block": block, "wgrad_KMN": [K, M, N], "buffer_sets": N_SETS},
+        "codec_frac_hbm": round(codec_gbs / HBM_PEAK_GBS, 4),
+        "wgrad_tflops": round(wgrad_tflops, 2),
+        "wgrad_frac_mfma": round(wgrad_tflops / BF16_PEAK_TFLOPS, 4),
+        "coeff_tok_s": round(coeff_tok_s, 1),
+        "kernel_ms": {n: round(v, 5) for n, v in avg.items()},
+        "roofline": roofs[dominant],
+        "rooflines": roofs,
+    }
+
+    if not args.no_cpu_baseline:
+        progress("timing the oracle on the host")
+        out["cpu_baseline"] = cpu_baseline(args, sets[0], w, block, code)
+    print(json.dumps(out))
+    return 0
+
+
+def cpu_baseline(args, st, w, block, code):
+    """The oracle (plain single-threaded C, as it stands) timed on this host on
+    a bounded sample of the same workload: compress (with row sums) and
+    decompress of the first --cpu-rows MLP rows and 4x as many hidden rows,
+    copied from the device byte for byte; plus the GRPO coefficients of the
+    full microbatch and a 128x128 corner of the wgrad, reported alongside."""
+    import numpy as np
+    import torch
+
+    import oracle
+
+    oracle.lib()
+    n_mlp, n_hid = args.cpu_rows, 4 * args.cpu_rows
+    xs = [st["keep"][0][0][:n_hid], st["keep"][1][0][:n_mlp]]
+    xs = [x.cpu().contiguous().view(torch.int16).numpy().view(np.uint16) for x in xs]
+    total = 0
+    t0 = time.perf_counter()
+    for x in xs:
+        c, s = oracle.quantize(x, code, block)
+        xh = oracle.dequantize(c, s, code, block)
+        oracle.row_stats(x, xh)
+        cb, db = codec_bytes(x.shape[0], x.shape[1], block, stats=True)
+        total += cb + db
+    dt_codec = time.perf_counter() - t0
+
+    b = st["grpo_host"]
+    t0 = time.perf_counter()
+    oracle.grpo_coeffs(b.rewards, b.logp_new, b.logp_old, None, None, b.P, b.G, b.T)
+    dt_grpo = time.perf_counter() - t0
+
+    K = st["wc"].shape[0]
+    wc = st["wc"][:, :128].cpu().contiguous().numpy()
+    ws = st["ws"][:, :1].cpu().contiguous().numpy()
+    dy = st["dy"][:, :128].cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+    t0 = time.perf_counter()
+    oracle.wgrad(wc, ws, code, block, dy, variant=0)
+    dt_w = time.perf_counter() - t0
+    return {
+        "value": round(total / dt_codec / 1e9, 4),
+        "unit": "GB/s",
+        "cores": 1,
+        "kind": "oracle",
+        "sample": f"compress+decompress of {n_hid}x{xs[0].shape[1]} hidden and "
+                  f"{n_mlp}x{xs[1].shape[1]} MLP rows (fp8-e4m3 1x{block}); "
+                  f"{dt_codec:.1f} s",
+        "coeff_tok_s": round(b.P * b.G * b.T / dt_grpo, 1),
+        "wgrad_tflops": round(2.0 * K * 128 * 128 / dt_w / 1e12, 6),
+        "wgrad_sample": f"dW[0:128, 0:128] over K={K} in fp64, {dt_w:.1f} s",
+    }
+
+
+if __name__ == "__main__":
+    sys.exit(main())

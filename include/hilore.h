@@ -1,0 +1,189 @@
+/*
+ * hilore.h -- C-ABI of the HiLoRe hot path on AMD Instinct MI355X (gfx950).
+ *
+ * HiLoRe ("HiLoRe: What to Store, Compress, or Recompute for Efficient GRPO
+ * Training") decides, for every saved activation unit of a GRPO actor update,
+ * whether to keep it in training precision (H), keep a low-precision copy (L)
+ * or recompute it (R).  Per microbatch (Algorithm 1) the data-parallel work is:
+ *   after forward   encode the L candidates                 -> hilore_compress
+ *   Coefficients    per-token GRPO loss coefficients omega  -> hilore_grpo_coeffs
+ *   Exposure, psi   per-unit exposure and risk              -> hilore_unit_exposure_risk
+ *   in backward     reconstruct L units                     -> hilore_decompress
+ *                   and consume them in the weight gradient -> hilore_dequant_wgrad
+ *
+ * Conventions shared by every entry point:
+ *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The
+ *     library never allocates, frees or retains memory, and keeps no state
+ *     between calls.  hilore_unit_desc arrays are HOST memory, read during the
+ *     call only.
+ *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
+ *     All work is enqueued on it without a host synchronisation; outputs are
+ *     valid once the stream reaches them.
+ *   - Every argument is validated before anything is launched: on an error
+ *     nothing is enqueued and no output is touched.  Validation touches no
+ *     device state, so argument errors are reported even without a GPU.
+ *   - bf16 tensors are passed as uint16_t* (raw bit patterns).
+ *   - Alignment: every tensor pointer must be 16-byte aligned.
+ *   - The functions are re-entrant; calls on different streams may run
+ *     concurrently.  No C++ exception crosses this interface.
+ *   - Results do not depend on the launch configuration: every reduction is
+ *     done in a fixed order, with no floating-point atomics.
+ */
+#ifndef HILORE_H
+#define HILORE_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum hilore_status {
+  HILORE_OK = 0,
+  HILORE_ERR_INVALID_ARG = 1, /* null pointer, negative size, bad enum value      */
+  HILORE_ERR_ALIGNMENT = 2,   /* pointer not 16-byte aligned, or bad row stride    */
+  HILORE_ERR_UNSUPPORTED = 3, /* valid but unsupported shape (e.g. G > 64)         */
+  HILORE_ERR_HIP = 5          /* a HIP launch failed (hipGetLastError)             */
+} hilore_status;
+
+typedef enum hilore_code {
+  HILORE_CODE_INT8 = 0,       /* two's-complement int8, symmetric range [-127, 127] */
+  HILORE_CODE_FP8_E4M3FN = 1  /* OCP E4M3FN (torch.float8_e4m3fn), max 448          */
+} hilore_code;
+
+/* One recovery unit: one saved bf16 activation tensor that receives a single
+ * H/L/R action across all its tokens (Sec. 3.4).  Rows are tokens of the
+ * microbatch, columns are features; blocks of `block` consecutive columns of
+ * one row share one fp32 scale.
+ *   x          bf16 [rows, cols], row stride ld elements (ld >= cols, ld % 8 == 0)
+ *   codes      [rows, cols] dense, one byte per element
+ *   scales     fp32 [rows, cols / block] dense
+ *   xhat       bf16 [rows, cols] dense: output of hilore_decompress
+ *   row_ss_x   fp32 [rows] or NULL: per-row sum of x^2
+ *   row_ss_err fp32 [rows] or NULL: per-row sum of (xhat - x)^2
+ * Each entry point reads only the fields it names. */
+typedef struct hilore_unit_desc {
+  const uint16_t *x;
+  void *codes;
+  float *scales;
+  uint16_t *xhat;
+  float *row_ss_x;
+  float *row_ss_err;
+  int64_t rows;
+  int64_t cols;
+  int64_t ld;
+} hilore_unit_desc;
+
+/* Human-readable name of a status code (static storage; never NULL). */
+const char *hilore_status_string(int status);
+
+/* Library version as 10000 * major + 100 * minor + patch. */
+int hilore_version(void);
+
+/*
+ * GRPO update quantities for P prompts x G responses x T token slots
+ * (Sec. 3.1 Eq. grpo-objective; Sec. 3.2 Eq. update-coefficient; the K3 KL
+ * derivative in the proof of Prop. 1; advantages as in App. D.1.1).
+ *
+ *   rewards  f32 [P*G]          response rewards, prompt-major (group i = rows iG..iG+G-1)
+ *   logp_new f32 [P*G*T]        s_t, current-policy log-prob of each slot (response-major)
+ *   logp_old f32 [P*G*T]        s_t^old
+ *   logp_ref f32 [P*G*T]        s_t^ref; may be NULL only when beta == 0
+ *   mask     u8  [P*G*T]        update mask m_t (nonzero = valid); NULL = all valid
+ *   clip_eps                    clipping radius eps (> 0, < 1)
+ *   adv_eps                     advantage stabiliser (the paper uses 1e-6)
+ *   beta                        K3 KL weight (>= 0)
+ *   n_norm                      N, the normaliser: > 0 uses this value (all valid tokens of
+ *                               the complete rollout batch); <= 0 uses the number of valid
+ *                               slots in this call
+ * Outputs (device):
+ *   adv      f32 [P*G]          A = (R - mean_group) / (population std_group + adv_eps),
+ *                               group sums formed as a pairwise tree over a power-of-two
+ *                               padding of the group (so the result is reproducible bit
+ *                               for bit)
+ *   ratio    f32 [P*G*T] or NULL  r_t = exp(s_t - s_t^old)
+ *   flags    u8  [P*G*T]        bit0: m_t and chi_t (policy term active);
+ *                               bit1: m_t and A != 0 and not chi_t (clipped)
+ *   coeff    f32 [P*G*T]        omega_t = (m_t / N) (-chi_t r_t A - beta expm1(s_ref - s_t));
+ *                               0 where m_t = 0 or N = 0
+ * chi_t is decided in log-ratio space: delta = s_t - s_t^old (fp32), chi = delta <= log1p(eps)
+ * when A >= 0, else delta >= log1p(-eps), both thresholds rounded to fp32.
+ * Limits: 1 <= G <= 64, P >= 0, T >= 0, P*G*T < 2^31.
+ */
+hilore_status hilore_grpo_coeffs(const float *rewards, const float *logp_new,
+                                 const float *logp_old, const float *logp_ref,
+                                 const uint8_t *mask, int P, int G, int T, float clip_eps,
+                                 float adv_eps, float beta, double n_norm, float *adv,
+                                 float *ratio, uint8_t *flags, float *coeff, void *stream);
+
+/*
+ * Blockwise absmax encode of the L candidates after forward (App. B.1 Eq.
+ * fp8-roundtrip, in the scaled reading: one fp32 scale per 1 x block run of a
+ * row; App. B.3 "post-forward encoding").  For every block, with Q = 127
+ * (int8) or 448 (E4M3FN) and amax = max |x| over the block:
+ *   amax < 2^-64  -> scale 0 and all codes 0;
+ *   otherwise      s = amax / Q and r = Q / amax (IEEE fp32 quotients),
+ *                  code = RNE(x * r) (int8: clamped to [-127,127]; E4M3FN: saturating),
+ *                  scale = s.
+ * With row_ss_x / row_ss_err non-NULL the same pass also writes, per row, the
+ * fp32 sums of x^2 (for the token RMS weights of Eq. activation-token-weights)
+ * and of (xhat - x)^2 with xhat = bf16(value(code) * s) (the reconstruction
+ * error of Eq. app-calibration-error), accumulated in a fixed order.
+ *   units[n_units]  host array; uses x, codes, scales, row_ss_x, row_ss_err, rows, cols, ld
+ *   block           32, 64, 128 or 256; every unit needs cols % block == 0
+ * All units of one call are encoded on `stream`; they may differ in shape.
+ */
+hilore_status hilore_compress(const hilore_unit_desc *units, int n_units, int code, int block,
+                              void *stream);
+
+/*
+ * Reconstruction of L units for backward (App. B.1 Eq. fp8-roundtrip, the cast
+ * back to bf16): xhat = bf16_RNE(value(code) * scale), elementwise.
+ *   units[n_units]  host array; uses codes, scales, xhat, rows, cols
+ */
+hilore_status hilore_decompress(const hilore_unit_desc *units, int n_units, int code,
+                                int block, void *stream);
+
+/*
+ * Per-unit exposure and risk for one microbatch (App. B.1 Eqs.
+ * activation-token-weights, mlp-weighted-exposure, app-calibration-error;
+ * Sec. 3.4 Eq. token-weighted-risk).  T = rows with a nonzero mask byte.
+ *   coeff    f32 [rows]  omega_t aligned to activation rows (zero on prompt/padding rows)
+ *   mask     u8  [rows]  valid response tokens T; NULL = all rows
+ *   units[n_units]       host array; uses row_ss_x, row_ss_err, rows (== rows), cols
+ * For each unit u, with a_t = sqrt(ss_x_t / cols):
+ *   exposure[u] = sum_{t in T} |omega_t| (a_t + eps_alpha) / (mean_{s in T} a_s + eps_alpha)
+ *   risk[u]     = sum_{t in T} |omega_t| sqrt(ss_err_t)
+ *   rel_err[u]  = sqrt(sum_t ss_err_t) / (sqrt(sum_t ss_x_t) + eps_rel)   (all rows)
+ * exposure and risk are 0 when T is empty.  Outputs are device f32 [n_units].
+ * The calibrated risk of App. B.1 Eq. app-risk-score is kappa * exposure * mean rel_err
+ * and the additive distortion of Eq. app-distortion sums it over L units; both are
+ * host-side scalar steps.
+ */
+hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask, int64_t rows,
+                                        const hilore_unit_desc *units, int n_units,
+                                        float eps_alpha, float eps_rel, float *exposure,
+                                        float *risk, float *rel_err, void *stream);
+
+/*
+ * Weight gradient of a linear layer whose saved input is an L unit, with the
+ * reconstruction fused into the GEMM's tile load (the full-parameter setting
+ * of App. D "full-parameter" experiments; accumulated over microbatches as in
+ * App. D.1.1):
+ *   dW[i][j] (+)= sum_t xhat[t][i] * dY[t][j],  xhat = bf16_RNE(value(code[t][i]) * scale[t][i/block])
+ *   x_codes  [K, M] one byte per element; x_scales f32 [K, M / block]
+ *   dy       bf16 [K, N]; dw f32 [M, N] row-major (the transpose of a [N, M] weight's layout)
+ *   accumulate: 0 overwrites dw, 1 adds to it
+ * bf16 x bf16 products, fp32 accumulation (MFMA).  xhat is never written to memory.
+ * Limits: M % block == 0, M % 8 == 0, N % 8 == 0, K >= 0 (K = 0 writes zeros or leaves dw).
+ */
+hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, int code,
+                                   int block, const uint16_t *dy, float *dw, int64_t K,
+                                   int64_t M, int64_t N, int accumulate, void *stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* HILORE_H */

@@ -1,0 +1,250 @@
+// C-ABI layer of libhilore: argument validation and dispatch to the gfx950
+// kernels.  Every check runs before anything is enqueued and touches no
+// device state, so invalid calls fail the same way with or without a GPU.
+#include "hilore.h"
+
+#include <hip/hip_runtime.h>
+
+#include <cmath>
+#include <cstdint>
+
+#include "hilore_internal.hpp"
+
+namespace {
+
+using hilore::CodecBatch;
+using hilore::CodecUnit;
+
+bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) == 0; }
+
+bool valid_block(int block) { return block == 32 || block == 64 || block == 128 || block == 256; }
+
+bool valid_code(int code) { return code == HILORE_CODE_INT8 || code == HILORE_CODE_FP8_E4M3FN; }
+
+hilore_status hip_status(hipError_t e) { return e == hipSuccess ? HILORE_OK : HILORE_ERR_HIP; }
+
+// Check the fields of one unit that an entry point reads.
+enum UnitUse : unsigned {
+  kUseX = 1u, kUseCodes = 2u, kUseScales = 4u, kUseXhat = 8u, kUseStats = 16u, kNeedStats = 32u
+};
+
+hilore_status check_unit(const hilore_unit_desc &u, int block, unsigned use) {
+  if (u.rows < 0 || u.cols < 0) return HILORE_ERR_INVALID_ARG;
+  if (block > 0 && u.cols % block != 0) return HILORE_ERR_UNSUPPORTED;
+  if (u.rows == 0 || u.cols == 0) return HILORE_OK;
+  if ((use & kUseX) != 0) {
+    if (!u.x) return HILORE_ERR_INVALID_ARG;
+    if (u.ld < u.cols) return HILORE_ERR_INVALID_ARG;
+    if (u.ld % 8 != 0 || !aligned16(u.x)) return HILORE_ERR_ALIGNMENT;
+  }
+  if ((use & kUseCodes) != 0) {
+    if (!u.codes) return HILORE_ERR_INVALID_ARG;
+    if (!aligned16(u.codes)) return HILORE_ERR_ALIGNMENT;
+  }
+  if ((use & kUseScales) != 0) {
+    if (!u.scales) return HILORE_ERR_INVALID_ARG;
+    if (!aligned16(u.scales)) return HILORE_ERR_ALIGNMENT;
+  }
+  if ((use & kUseXhat) != 0) {
+    if (!u.xhat) return HILORE_ERR_INVALID_ARG;
+    if (!aligned16(u.xhat)) return HILORE_ERR_ALIGNMENT;
+  }
+  if ((use & (kUseStats | kNeedStats)) != 0) {
+    if ((use & kNeedStats) != 0 && (!u.row_ss_x || !u.row_ss_err)) return HILORE_ERR_INVALID_ARG;
+    if ((u.row_ss_x && !aligned16(u.row_ss_x)) || (u.row_ss_err && !aligned16(u.row_ss_err)))
+      return HILORE_ERR_ALIGNMENT;
+  }
+  return HILORE_OK;
+}
+
+// Validate every unit, then launch in batches of kUnitsPerLaunch.
+template <typename Launch>
+hilore_status run_codec(const hilore_unit_desc *units, int n_units, int code, int block,
+                        unsigned use, bool stats, Launch launch) {
+  if (n_units < 0) return HILORE_ERR_INVALID_ARG;
+  if (n_units == 0) return HILORE_OK;
+  if (!units) return HILORE_ERR_INVALID_ARG;
+  if (!valid_code(code)) return HILORE_ERR_INVALID_ARG;
+  if (!valid_block(block)) return HILORE_ERR_UNSUPPORTED;
+  for (int i = 0; i < n_units; ++i) {
+    const hilore_status st = check_unit(units[i], block, use);
+    if (st != HILORE_OK) return st;
+  }
+  for (int first = 0; first < n_units; first += hilore::kUnitsPerLaunch) {
+    CodecBatch b{};
+    int64_t rows = 0;
+    bool any_stats = false;
+    for (int i = first; i < n_units && b.n < hilore::kUnitsPerLaunch; ++i) {
+      const hilore_unit_desc &u = units[i];
+      if (u.rows == 0 || u.cols == 0) continue;
+      CodecUnit &c = b.u[b.n];
+      c.x = u.x;
+      c.codes = static_cast<uint8_t *>(u.codes);
+      c.scales = u.scales;
+      c.xhat = u.xhat;
+      c.ss_x = stats ? u.row_ss_x : nullptr;
+      c.ss_err = stats ? u.row_ss_err : nullptr;
+      c.rows = u.rows;
+      c.cols = u.cols;
+      c.ld = u.ld;
+      any_stats = any_stats || c.ss_x || c.ss_err;
+      b.row_begin[b.n] = rows;
+      rows += u.rows;
+      ++b.n;
+    }
+    if (b.n == 0) continue;
+    b.row_begin[b.n] = rows;
+    b.stats = any_stats ? 1 : 0;
+    const hilore_status st = hip_status(launch(b));
+    if (st != HILORE_OK) return st;
+  }
+  return HILORE_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+const char *hilore_status_string(int status) {
+  switch (status) {
+    case HILORE_OK: return "HILORE_OK";
+    case HILORE_ERR_INVALID_ARG: return "HILORE_ERR_INVALID_ARG";
+    case HILORE_ERR_ALIGNMENT: return "HILORE_ERR_ALIGNMENT";
+    case HILORE_ERR_UNSUPPORTED: return "HILORE_ERR_UNSUPPORTED";
+    case HILORE_ERR_HIP: return "HILORE_ERR_HIP";
+    default: return "HILORE_ERR_UNKNOWN";
+  }
+}
+
+int hilore_version(void) { return 10000; }
+
+hilore_status hilore_grpo_coeffs(const float *rewards, const float *logp_new,
+                                 const float *logp_old, const float *logp_ref,
+                                 const uint8_t *mask, int P, int G, int T, float clip_eps,
+                                 float adv_eps, float beta, double n_norm, float *adv,
+                                 float *ratio, uint8_t *flags, float *coeff, void *stream) {
+  if (P < 0 || T < 0 || G < 1) return HILORE_ERR_INVALID_ARG;
+  if (G > 64) return HILORE_ERR_UNSUPPORTED;
+  const int64_t R = (int64_t)P * G;
+  const int64_t n = R * (int64_t)T;
+  if (n >= (int64_t(1) << 31) || R >= (int64_t(1) << 31)) return HILORE_ERR_UNSUPPORTED;
+  if (!(clip_eps > 0.0f && clip_eps < 1.0f) || !(adv_eps >= 0.0f) || !(beta >= 0.0f) ||
+      !std::isfinite(beta) || std::isnan(n_norm))
+    return HILORE_ERR_INVALID_ARG;
+  if (R == 0) return HILORE_OK;
+  if (!rewards || !adv) return HILORE_ERR_INVALID_ARG;
+  if (!aligned16(rewards) || !aligned16(adv)) return HILORE_ERR_ALIGNMENT;
+  if (n > 0) {
+    if (!logp_new || !logp_old || !flags || !coeff) return HILORE_ERR_INVALID_ARG;
+    if (beta != 0.0f && !logp_ref) return HILORE_ERR_INVALID_ARG;
+    const void *ptrs[] = {logp_new, logp_old, logp_ref, mask, ratio, flags, coeff};
+    for (const void *p : ptrs)
+      if (p && !aligned16(p)) return HILORE_ERR_ALIGNMENT;
+  }
+  hilore::GrpoArgs a{};
+  a.rewards = rewards;
+  a.logp_new = logp_new;
+  a.logp_old = logp_old;
+  a.logp_ref = beta != 0.0f ? logp_ref : nullptr;
+  a.mask = mask;
+  a.adv = adv;
+  a.ratio = ratio;
+  a.coeff = coeff;
+  a.flags = flags;
+  a.P = P;
+  a.G = G;
+  a.T = T;
+  a.hi = (float)std::log1p((double)clip_eps);
+  a.lo = (float)std::log1p(-(double)clip_eps);
+  a.adv_eps = adv_eps;
+  a.beta = beta;
+  a.count_mask = n_norm > 0.0 ? 0 : 1;
+  a.inv_n = n_norm > 0.0 ? (float)(1.0 / n_norm) : 0.0f;
+  return hip_status(hilore::launch_grpo(a, static_cast<hipStream_t>(stream)));
+}
+
+hilore_status hilore_compress(const hilore_unit_desc *units, int n_units, int code, int block,
+                              void *stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return run_codec(units, n_units, code, block, kUseX | kUseCodes | kUseScales | kUseStats, true,
+                   [&](const CodecBatch &b) { return hilore::launch_compress(b, code, block, s); });
+}
+
+hilore_status hilore_decompress(const hilore_unit_desc *units, int n_units, int code,
+                                int block, void *stream) {
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  return run_codec(units, n_units, code, block, kUseCodes | kUseScales | kUseXhat, false,
+                   [&](const CodecBatch &b) { return hilore::launch_decompress(b, code, block, s); });
+}
+
+hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask, int64_t rows,
+                                        const hilore_unit_desc *units, int n_units,
+                                        float eps_alpha, float eps_rel, float *exposure,
+                                        float *risk, float *rel_err, void *stream) {
+  if (rows < 0 || n_units < 0) return HILORE_ERR_INVALID_ARG;
+  if (!(eps_alpha >= 0.0f) || !(eps_rel >= 0.0f)) return HILORE_ERR_INVALID_ARG;
+  if (n_units == 0) return HILORE_OK;
+  if (!units || !exposure || !risk || !rel_err) return HILORE_ERR_INVALID_ARG;
+  if (rows >= (int64_t(1) << 24)) return HILORE_ERR_UNSUPPORTED;
+  if (rows > 0 && !coeff) return HILORE_ERR_INVALID_ARG;
+  const void *ptrs[] = {coeff, mask, exposure, risk, rel_err};
+  for (const void *p : ptrs)
+    if (p && !aligned16(p)) return HILORE_ERR_ALIGNMENT;
+  for (int i = 0; i < n_units; ++i) {
+    const hilore_unit_desc &u = units[i];
+    if (u.rows != rows || u.cols <= 0) return HILORE_ERR_INVALID_ARG;
+    if (rows > 0) {
+      const hilore_status st = check_unit(u, 0, kNeedStats);
+      if (st != HILORE_OK) return st;
+    }
+  }
+  hipStream_t s = static_cast<hipStream_t>(stream);
+  for (int first = 0; first < n_units; first += hilore::kRiskUnitsPerLaunch) {
+    hilore::RiskBatch b{};
+    b.coeff = coeff;
+    b.mask = mask;
+    b.rows = rows;
+    b.eps_alpha = eps_alpha;
+    b.eps_rel = eps_rel;
+    b.exposure = exposure + first;
+    b.risk = risk + first;
+    b.rel_err = rel_err + first;
+    for (int i = first; i < n_units && b.n < hilore::kRiskUnitsPerLaunch; ++i) {
+      b.u[b.n].ss_x = units[i].row_ss_x;
+      b.u[b.n].ss_err = units[i].row_ss_err;
+      b.u[b.n].inv_cols = (float)(1.0 / (double)units[i].cols);
+      ++b.n;
+    }
+    const hilore_status st = hip_status(hilore::launch_exposure_risk(b, s));
+    if (st != HILORE_OK) return st;
+  }
+  return HILORE_OK;
+}
+
+hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, int code,
+                                   int block, const uint16_t *dy, float *dw, int64_t K,
+                                   int64_t M, int64_t N, int accumulate, void *stream) {
+  if (K < 0 || M < 0 || N < 0) return HILORE_ERR_INVALID_ARG;
+  if (!valid_code(code)) return HILORE_ERR_INVALID_ARG;
+  if (!valid_block(block)) return HILORE_ERR_UNSUPPORTED;
+  if (M % block != 0 || M % 8 != 0 || N % 8 != 0) return HILORE_ERR_UNSUPPORTED;
+  if (M / 256 + 1 > (1 << 14) || N / 256 + 1 > (1 << 14)) return HILORE_ERR_UNSUPPORTED;
+  if (M == 0 || N == 0) return HILORE_OK;
+  if (!dw) return HILORE_ERR_INVALID_ARG;
+  if (K > 0 && (!x_codes || !x_scales || !dy)) return HILORE_ERR_INVALID_ARG;
+  const void *ptrs[] = {x_codes, x_scales, dy, dw};
+  for (const void *p : ptrs)
+    if (p && !aligned16(p)) return HILORE_ERR_ALIGNMENT;
+  hilore::WgradArgs a{};
+  a.codes = static_cast<const uint8_t *>(x_codes);
+  a.scales = x_scales;
+  a.dy = dy;
+  a.dw = dw;
+  a.K = K;
+  a.M = M;
+  a.N = N;
+  a.accumulate = accumulate ? 1 : 0;
+  return hip_status(hilore::launch_wgrad(a, code, block, static_cast<hipStream_t>(stream)));
+}
+
+}  // extern "C"

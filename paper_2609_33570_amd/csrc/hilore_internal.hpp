@@ -1,0 +1,82 @@
+// Internal interface between the C-ABI layer (abi.cpp) and the gfx950 kernels.
+// Not installed; the public interface is include/hilore.h.
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stdint.h>
+
+namespace hilore {
+
+constexpr int kCodeInt8 = 0;
+constexpr int kCodeE4M3 = 1;
+
+// One unit as the codec kernels see it (a validated copy of hilore_unit_desc).
+struct CodecUnit {
+  const uint16_t *x;
+  uint8_t *codes;
+  float *scales;
+  uint16_t *xhat;
+  float *ss_x;
+  float *ss_err;
+  int64_t rows;
+  int64_t cols;
+  int64_t ld;
+};
+
+// Units encoded/decoded by one launch travel by value in the kernel
+// arguments, so a call needs no device workspace and no host->device copy.
+constexpr int kUnitsPerLaunch = 16;
+struct CodecBatch {
+  CodecUnit u[kUnitsPerLaunch];
+  int64_t row_begin[kUnitsPerLaunch + 1];  // prefix sum of rows over u[]
+  int n;
+  int stats;  // compress: write row sums
+};
+
+hipError_t launch_compress(const CodecBatch &b, int code, int block, hipStream_t s);
+hipError_t launch_decompress(const CodecBatch &b, int code, int block, hipStream_t s);
+
+struct RiskUnit {
+  const float *ss_x;
+  const float *ss_err;
+  float inv_cols;  // 1 / d_u
+};
+constexpr int kRiskUnitsPerLaunch = 32;
+struct RiskBatch {
+  RiskUnit u[kRiskUnitsPerLaunch];
+  float *exposure;  // already offset to the first unit of this launch
+  float *risk;
+  float *rel_err;
+  const float *coeff;
+  const uint8_t *mask;
+  int64_t rows;
+  float eps_alpha;
+  float eps_rel;
+  int n;
+};
+hipError_t launch_exposure_risk(const RiskBatch &b, hipStream_t s);
+
+struct GrpoArgs {
+  const float *rewards, *logp_new, *logp_old, *logp_ref;
+  const uint8_t *mask;
+  float *adv, *ratio, *coeff;
+  uint8_t *flags;
+  int P, G, T;
+  float hi, lo;       // fp32 log1p(+eps), log1p(-eps)
+  float adv_eps, beta;
+  float inv_n;        // 1/N when N is given
+  int count_mask;     // N = number of valid slots in this call
+};
+hipError_t launch_grpo(const GrpoArgs &a, hipStream_t s);
+
+struct WgradArgs {
+  const uint8_t *codes;
+  const float *scales;
+  const uint16_t *dy;
+  float *dw;
+  int64_t K, M, N;
+  int accumulate;
+};
+hipError_t launch_wgrad(const WgradArgs &a, int code, int block, hipStream_t s);
+
+}  // namespace hilore

@@ -1,0 +1,177 @@
+"""Thin Python binding of libhilore (the C-ABI in include/hilore.h).
+
+Argument marshalling only: every step runs in the library's HIP kernels.
+Tensors are torch tensors on the GPU (torch provides device memory and the
+stream); each function passes their data pointers and the current stream to
+the C entry point of the same name and raises HiloreError on a non-zero
+status.  There is no fallback: without libhilore.so the import fails.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+from typing import Optional, Sequence
+
+_PKG = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_PKG, "libhilore.so")
+
+HILORE_OK = 0
+HILORE_ERR_INVALID_ARG = 1
+HILORE_ERR_ALIGNMENT = 2
+HILORE_ERR_UNSUPPORTED = 3
+HILORE_ERR_HIP = 5
+
+HILORE_CODE_INT8 = 0
+HILORE_CODE_FP8_E4M3FN = 1
+CODES = {"int8": HILORE_CODE_INT8, "e4m3fn": HILORE_CODE_FP8_E4M3FN}
+
+
+class HiloreError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        self.status = status
+        super().__init__(f"{fn} failed: {status_string(status)} ({status})")
+
+
+class hilore_unit_desc(ctypes.Structure):
+    _fields_ = [
+        ("x", ctypes.c_void_p),
+        ("codes", ctypes.c_void_p),
+        ("scales", ctypes.c_void_p),
+        ("xhat", ctypes.c_void_p),
+        ("row_ss_x", ctypes.c_void_p),
+        ("row_ss_err", ctypes.c_void_p),
+        ("rows", ctypes.c_int64),
+        ("cols", ctypes.c_int64),
+        ("ld", ctypes.c_int64),
+    ]
+
+
+_lib = None
+
+
+def load() -> ctypes.CDLL:
+    """Load libhilore.so (built in-tree by __graft_entry__.build())."""
+    global _lib
+    if _lib is not None:
+        return _lib
+    if not os.path.exists(LIB_PATH):
+        raise ImportError(f"{LIB_PATH} is not built; run __graft_entry__.build() first")
+    L = ctypes.CDLL(LIB_PATH)
+    P = ctypes.c_void_p
+    i32 = ctypes.c_int
+    i64 = ctypes.c_int64
+    f32 = ctypes.c_float
+    f64 = ctypes.c_double
+    sig = {
+        "hilore_status_string": (ctypes.c_char_p, [i32]),
+        "hilore_version": (i32, []),
+        "hilore_grpo_coeffs": (i32, [P, P, P, P, P, i32, i32, i32, f32, f32, f32, f64,
+                                     P, P, P, P, P]),
+        "hilore_compress": (i32, [P, i32, i32, i32, P]),
+        "hilore_decompress": (i32, [P, i32, i32, i32, P]),
+        "hilore_unit_exposure_risk": (i32, [P, P, i64, P, i32, f32, f32, P, P, P, P]),
+        "hilore_dequant_wgrad": (i32, [P, P, i32, i32, P, P, i64, i64, i64, i32, P]),
+    }
+    for name, (res, args) in sig.items():
+        fn = getattr(L, name)
+        fn.restype = res
+        fn.argtypes = args
+    _lib = L
+    return L
+
+
+def status_string(status: int) -> str:
+    return load().hilore_status_string(int(status)).decode()
+
+
+def version() -> int:
+    return load().hilore_version()
+
+
+def _check(fn: str, status: int) -> None:
+    if status != HILORE_OK:
+        raise HiloreError(fn, status)
+
+
+def _p(t) -> Optional[int]:
+    """Data pointer of a tensor (None -> NULL)."""
+    if t is None:
+        return None
+    return t.data_ptr()
+
+
+def _stream(stream) -> Optional[int]:
+    if stream is not None:
+        return int(stream)
+    import torch
+
+    return torch.cuda.current_stream().cuda_stream
+
+
+def _code(code) -> int:
+    return CODES[code] if isinstance(code, str) else int(code)
+
+
+def unit_desc(x=None, codes=None, scales=None, xhat=None, row_ss_x=None, row_ss_err=None,
+              rows=None, cols=None, ld=None) -> hilore_unit_desc:
+    """Descriptor of one unit from torch tensors (shapes taken from the tensors
+    when not given: x is [rows, ld] with ld = row stride; codes [rows, cols])."""
+    ref = x if x is not None else (codes if codes is not None else xhat)
+    if rows is None:
+        rows = ref.shape[0] if ref is not None else (row_ss_x.shape[0] if row_ss_x is not None else 0)
+    if cols is None:
+        if codes is not None:
+            cols = codes.shape[1]
+        elif xhat is not None:
+            cols = xhat.shape[1]
+        else:
+            cols = x.shape[1]
+    if ld is None:
+        ld = x.stride(0) if x is not None else cols
+    return hilore_unit_desc(_p(x), _p(codes), _p(scales), _p(xhat), _p(row_ss_x),
+                            _p(row_ss_err), int(rows), int(cols), int(ld))
+
+
+def _desc_array(units: Sequence[hilore_unit_desc]):
+    arr = (hilore_unit_desc * max(1, len(units)))(*units)
+    return arr, len(units)
+
+
+# ---------------------------------------------------------------- entry points --
+def hilore_grpo_coeffs(rewards, logp_new, logp_old, logp_ref, mask, P, G, T, clip_eps,
+                       adv_eps, beta, n_norm, adv, ratio, flags, coeff, stream=None):
+    st = load().hilore_grpo_coeffs(_p(rewards), _p(logp_new), _p(logp_old), _p(logp_ref),
+                                   _p(mask), int(P), int(G), int(T), float(clip_eps),
+                                   float(adv_eps), float(beta), float(n_norm), _p(adv),
+                                   _p(ratio), _p(flags), _p(coeff), _stream(stream))
+    _check("hilore_grpo_coeffs", st)
+
+
+def hilore_compress(units: Sequence[hilore_unit_desc], code, block: int, stream=None):
+    arr, n = _desc_array(units)
+    _check("hilore_compress",
+           load().hilore_compress(arr, n, _code(code), int(block), _stream(stream)))
+
+
+def hilore_decompress(units: Sequence[hilore_unit_desc], code, block: int, stream=None):
+    arr, n = _desc_array(units)
+    _check("hilore_decompress",
+           load().hilore_decompress(arr, n, _code(code), int(block), _stream(stream)))
+
+
+def hilore_unit_exposure_risk(coeff, mask, rows: int, units: Sequence[hilore_unit_desc],
+                              eps_alpha: float, eps_rel: float, exposure, risk, rel_err,
+                              stream=None):
+    arr, n = _desc_array(units)
+    _check("hilore_unit_exposure_risk",
+           load().hilore_unit_exposure_risk(_p(coeff), _p(mask), int(rows), arr, n,
+                                            float(eps_alpha), float(eps_rel), _p(exposure),
+                                            _p(risk), _p(rel_err), _stream(stream)))
+
+
+def hilore_dequant_wgrad(x_codes, x_scales, code, block: int, dy, dw, K: int, M: int, N: int,
+                         accumulate: bool = False, stream=None):
+    _check("hilore_dequant_wgrad",
+           load().hilore_dequant_wgrad(_p(x_codes), _p(x_scales), _code(code), int(block),
+                                       _p(dy), _p(dw), int(K), int(M), int(N),
+                                       1 if accumulate else 0, _stream(stream)))

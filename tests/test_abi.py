@@ -1,0 +1,163 @@
+"""The C-ABI library on the host: it loads, exports every entry point that
+include/hilore.h declares, and rejects invalid arguments before touching the
+device (so these checks run without a GPU)."""
+import ctypes
+import os
+import re
+
+import pytest
+
+from paper_2609_33570_amd import hilore
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "hilore.h")
+
+# A fake but 16-byte aligned "device" address: never dereferenced, because
+# every call below fails validation first.
+FAKE = 1 << 20
+
+
+@pytest.fixture(scope="module")
+def lib():
+    if not os.path.exists(hilore.LIB_PATH):
+        from paper_2609_33570_amd import _build
+
+        _build.build()
+    return hilore.load()
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(hilore_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_symbol(lib):
+    names = declared_functions()
+    assert {"hilore_grpo_coeffs", "hilore_compress", "hilore_decompress",
+            "hilore_unit_exposure_risk", "hilore_dequant_wgrad"} <= set(names)
+    for n in names:
+        assert hasattr(lib, n), n
+
+
+def test_status_strings_and_version(lib):
+    assert hilore.status_string(0) == "HILORE_OK"
+    assert hilore.status_string(3) == "HILORE_ERR_UNSUPPORTED"
+    assert hilore.status_string(99) == "HILORE_ERR_UNKNOWN"
+    assert hilore.version() >= 10000
+
+
+def grpo(lib, **kw):
+    a = dict(rewards=FAKE, logp_new=FAKE, logp_old=FAKE, logp_ref=None, mask=None, P=2, G=8,
+             T=16, clip_eps=0.2, adv_eps=1e-6, beta=0.0, n_norm=0.0, adv=FAKE, ratio=None,
+             flags=FAKE, coeff=FAKE)
+    a.update(kw)
+    return lib.hilore_grpo_coeffs(a["rewards"], a["logp_new"], a["logp_old"], a["logp_ref"],
+                                  a["mask"], a["P"], a["G"], a["T"], a["clip_eps"],
+                                  a["adv_eps"], a["beta"], a["n_norm"], a["adv"], a["ratio"],
+                                  a["flags"], a["coeff"], None)
+
+
+def test_grpo_validation(lib):
+    assert grpo(lib, G=65) == hilore.HILORE_ERR_UNSUPPORTED
+    assert grpo(lib, G=0) == hilore.HILORE_ERR_INVALID_ARG
+    assert grpo(lib, P=-1) == hilore.HILORE_ERR_INVALID_ARG
+    assert grpo(lib, T=-1) == hilore.HILORE_ERR_INVALID_ARG
+    assert grpo(lib, P=1 << 20, G=64, T=1 << 12) == hilore.HILORE_ERR_UNSUPPORTED
+    assert grpo(lib, clip_eps=0.0) == hilore.HILORE_ERR_INVALID_ARG
+    assert grpo(lib, clip_eps=1.0) == hilore.HILORE_ERR_INVALID_ARG
+    assert grpo(lib, beta=-1.0) == hilore.HILORE_ERR_INVALID_ARG
+    assert grpo(lib, beta=1e-3) == hilore.HILORE_ERR_INVALID_ARG  # logp_ref missing
+    assert grpo(lib, rewards=None) == hilore.HILORE_ERR_INVALID_ARG
+    assert grpo(lib, coeff=None) == hilore.HILORE_ERR_INVALID_ARG
+    assert grpo(lib, flags=None) == hilore.HILORE_ERR_INVALID_ARG
+    assert grpo(lib, logp_new=FAKE + 4) == hilore.HILORE_ERR_ALIGNMENT
+    assert grpo(lib, mask=FAKE + 8) == hilore.HILORE_ERR_ALIGNMENT
+    assert grpo(lib, P=0) == hilore.HILORE_OK  # nothing to do, nothing launched
+
+
+def unit(**kw):
+    d = dict(x=FAKE, codes=FAKE, scales=FAKE, xhat=FAKE, row_ss_x=None, row_ss_err=None,
+             rows=4, cols=256, ld=256)
+    d.update(kw)
+    return hilore.hilore_unit_desc(d["x"], d["codes"], d["scales"], d["xhat"], d["row_ss_x"],
+                                   d["row_ss_err"], d["rows"], d["cols"], d["ld"])
+
+
+def codec(lib, fn, units, code=0, block=128):
+    arr = (hilore.hilore_unit_desc * max(1, len(units)))(*units)
+    return getattr(lib, fn)(arr, len(units), code, block, None)
+
+
+@pytest.mark.parametrize("fn", ["hilore_compress", "hilore_decompress"])
+def test_codec_validation(lib, fn):
+    E = hilore
+    assert codec(lib, fn, [unit()], code=2) == E.HILORE_ERR_INVALID_ARG
+    assert codec(lib, fn, [unit()], block=48) == E.HILORE_ERR_UNSUPPORTED
+    assert codec(lib, fn, [unit()], block=512) == E.HILORE_ERR_UNSUPPORTED
+    assert codec(lib, fn, [unit(cols=200)], block=128) == E.HILORE_ERR_UNSUPPORTED
+    assert codec(lib, fn, [unit(rows=-1)]) == E.HILORE_ERR_INVALID_ARG
+    assert codec(lib, fn, [unit(codes=None)]) == E.HILORE_ERR_INVALID_ARG
+    assert codec(lib, fn, [unit(scales=None)]) == E.HILORE_ERR_INVALID_ARG
+    assert codec(lib, fn, [unit(scales=FAKE + 4)]) == E.HILORE_ERR_ALIGNMENT
+    # a bad unit anywhere in the list rejects the whole call
+    assert codec(lib, fn, [unit()] * 20 + [unit(codes=None)]) == E.HILORE_ERR_INVALID_ARG
+    assert getattr(lib, fn)(None, 1, 0, 128, None) == E.HILORE_ERR_INVALID_ARG
+    assert getattr(lib, fn)(None, -1, 0, 128, None) == E.HILORE_ERR_INVALID_ARG
+    assert getattr(lib, fn)(None, 0, 0, 128, None) == E.HILORE_OK
+    # empty units are skipped without a launch
+    assert codec(lib, fn, [unit(rows=0, codes=None, x=None, xhat=None)]) == E.HILORE_OK
+
+
+def test_compress_specific_validation(lib):
+    E = hilore
+    f = "hilore_compress"
+    assert codec(lib, f, [unit(x=None)]) == E.HILORE_ERR_INVALID_ARG
+    assert codec(lib, f, [unit(ld=128)]) == E.HILORE_ERR_INVALID_ARG
+    assert codec(lib, f, [unit(ld=260)]) == E.HILORE_ERR_ALIGNMENT
+    assert codec(lib, f, [unit(x=FAKE + 2)]) == E.HILORE_ERR_ALIGNMENT
+    assert codec(lib, f, [unit(row_ss_x=FAKE + 4)]) == E.HILORE_ERR_ALIGNMENT
+
+
+def test_decompress_specific_validation(lib):
+    assert codec(lib, "hilore_decompress", [unit(xhat=None)]) == hilore.HILORE_ERR_INVALID_ARG
+
+
+def risk(lib, units, rows=4, coeff=FAKE, mask=None, outs=(FAKE, FAKE, FAKE), eps=(1e-8, 1e-8)):
+    arr = (hilore.hilore_unit_desc * max(1, len(units)))(*units)
+    return lib.hilore_unit_exposure_risk(coeff, mask, rows, arr, len(units), eps[0], eps[1],
+                                         outs[0], outs[1], outs[2], None)
+
+
+def test_exposure_risk_validation(lib):
+    E = hilore
+    ok = unit(row_ss_x=FAKE, row_ss_err=FAKE)
+    assert risk(lib, [unit()]) == E.HILORE_ERR_INVALID_ARG          # row sums missing
+    assert risk(lib, [ok], rows=5) == E.HILORE_ERR_INVALID_ARG      # rows disagree
+    assert risk(lib, [ok], coeff=None) == E.HILORE_ERR_INVALID_ARG
+    assert risk(lib, [ok], outs=(None, FAKE, FAKE)) == E.HILORE_ERR_INVALID_ARG
+    assert risk(lib, [ok], mask=FAKE + 1) == E.HILORE_ERR_ALIGNMENT
+    assert risk(lib, [ok], eps=(-1.0, 1e-8)) == E.HILORE_ERR_INVALID_ARG
+    assert risk(lib, [unit(row_ss_x=FAKE, row_ss_err=FAKE, cols=0)]) == E.HILORE_ERR_INVALID_ARG
+    assert risk(lib, []) == E.HILORE_OK
+
+
+def wgrad(lib, **kw):
+    a = dict(x_codes=FAKE, x_scales=FAKE, code=1, block=128, dy=FAKE, dw=FAKE, K=256, M=512,
+             N=512, accumulate=0)
+    a.update(kw)
+    return lib.hilore_dequant_wgrad(a["x_codes"], a["x_scales"], a["code"], a["block"], a["dy"],
+                                    a["dw"], a["K"], a["M"], a["N"], a["accumulate"], None)
+
+
+def test_wgrad_validation(lib):
+    E = hilore
+    assert wgrad(lib, M=192) == E.HILORE_ERR_UNSUPPORTED        # M % block
+    assert wgrad(lib, N=100) == E.HILORE_ERR_UNSUPPORTED        # N % 8
+    assert wgrad(lib, block=100) == E.HILORE_ERR_UNSUPPORTED
+    assert wgrad(lib, code=7) == E.HILORE_ERR_INVALID_ARG
+    assert wgrad(lib, K=-1) == E.HILORE_ERR_INVALID_ARG
+    assert wgrad(lib, dw=None) == E.HILORE_ERR_INVALID_ARG
+    assert wgrad(lib, dy=None) == E.HILORE_ERR_INVALID_ARG
+    assert wgrad(lib, x_scales=FAKE + 4) == E.HILORE_ERR_ALIGNMENT
+    assert wgrad(lib, M=0) == E.HILORE_OK

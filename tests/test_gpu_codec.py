@@ -1,0 +1,156 @@
+"""GPU parity of hilore_compress / hilore_decompress against the oracle.
+
+Codes, scales and reconstructions bit for bit; per-row sums within 1e-5
+relative of the fp64 truth.  Covers both codes and all block sizes, rows that
+end mid-step (columns not a multiple of 512), strided rows, every finite
+bf16 value, every scale mantissa and a wide range of exponents, zero and
+tiny blocks, batches of more than one launch's worth of units, and
+repeatability.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_33570_amd import workloads as wl
+from gpu_util import assert_bytes_equal, assert_close, dev, filled, host
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_codec(hl, xs, code, block, stats=True, cols=None):
+    """Compress then decompress a list of host bf16 arrays [rows, ld] in one
+    batched call each; returns per unit (codes, scales, xhat, ss_x, ss_err)."""
+    units_c, units_d, bufs = [], [], []
+    for i, x in enumerate(xs):
+        rows, ld = x.shape
+        c = ld if cols is None else cols[i]
+        xd = dev(x)
+        codes = filled((rows, c), torch.uint8, 0xEE)
+        scales = filled((rows, c // block), torch.float32, float("nan"))
+        xhat = filled((rows, c), torch.int16, 0x7FC1)
+        ssx = filled((rows,), torch.float32, float("nan")) if stats else None
+        sse = filled((rows,), torch.float32, float("nan")) if stats else None
+        bufs.append((xd, codes, scales, xhat, ssx, sse))
+        units_c.append(hl.unit_desc(x=xd, codes=codes, scales=scales, row_ss_x=ssx,
+                                    row_ss_err=sse, rows=rows, cols=c, ld=ld))
+        units_d.append(hl.unit_desc(codes=codes, scales=scales, xhat=xhat, rows=rows, cols=c))
+    hl.hilore_compress(units_c, code, block)
+    hl.hilore_decompress(units_d, code, block)
+    torch.cuda.synchronize()
+    out = []
+    for xd, codes, scales, xhat, ssx, sse in bufs:
+        out.append((host(codes), host(scales), host(xhat).view(np.uint16),
+                    host(ssx) if stats else None, host(sse) if stats else None))
+    return out
+
+
+def check_unit(orc, x, res, code, block, cols=None, what=""):
+    codes, scales, xhat, ssx, sse = res
+    o_codes, o_scales = orc.quantize(x, code, block, cols=cols)
+    o_xhat = orc.dequantize(o_codes, o_scales, code, block)
+    assert_bytes_equal(codes, o_codes, f"{what} codes")
+    assert_bytes_equal(scales, o_scales, f"{what} scales")
+    assert_bytes_equal(xhat, o_xhat, f"{what} xhat")
+    if ssx is not None:
+        c = o_codes.shape[1]
+        o_ssx, o_sse = orc.row_stats(np.ascontiguousarray(x[:, :c]), o_xhat)
+        assert_close(ssx, o_ssx, f"{what} row sum x^2")
+        assert_close(sse, o_sse, f"{what} row sum err^2")
+
+
+@pytest.mark.parametrize("code", [0, 1], ids=["int8", "e4m3fn"])
+@pytest.mark.parametrize("block", [32, 64, 128, 256])
+def test_shapes_and_blocks(hl, orc, code, block):
+    shapes = [(192, 896 if 896 % block == 0 else 1024), (37, 2048), (5, 3 * block), (64, 4608)]
+    xs = [wl.activation_host(r, c, seed=100 + i, outliers=("channels", 0.005, 30.0))
+          for i, (r, c) in enumerate(shapes)]
+    res = gpu_codec(hl, xs, code, block)
+    for x, r, s in zip(xs, res, shapes):
+        check_unit(orc, x, r, code, block, what=f"{s}")
+
+
+def test_tiny_workload_int8(hl, orc):
+    """1024 x 896 bf16 N(0,1) with 1% of entries x20, int8 1x128."""
+    x = wl.activation_host(1024, 896, seed=wl.TINY.seed, outliers=("entries", 0.01, 20.0))
+    (res,) = gpu_codec(hl, [x], 0, 128)
+    check_unit(orc, x, res, 0, 128, what="tiny")
+
+
+@pytest.mark.parametrize("code", [0, 1], ids=["int8", "e4m3fn"])
+def test_strided_rows(hl, orc, code):
+    x = wl.activation_host(50, 768, seed=7, ld=1024)
+    (res,) = gpu_codec(hl, [x], code, 64, cols=[768])
+    check_unit(orc, x, res, code, 64, cols=768, what="strided")
+
+
+@pytest.mark.parametrize("code", [0, 1], ids=["int8", "e4m3fn"])
+def test_every_bf16_value(hl, orc, code):
+    """Every finite bf16 value, in blocks whose amax is a fixed anchor (or the
+    value itself when larger)."""
+    vals = np.arange(1 << 16, dtype=np.uint32)
+    vals = vals[(vals & 0x7F80) != 0x7F80].astype(np.uint16)
+    block = 32
+    n_per = block - 1
+    pad = (-vals.size) % n_per
+    vals = np.concatenate([vals, np.zeros(pad, np.uint16)]).reshape(-1, n_per)
+    x = np.empty((vals.shape[0], block), np.uint16)
+    x[:, 0] = wl.to_bf16_bits(np.float32([3.0]))[0]
+    x[:, 1:] = vals
+    rows = x.shape[0] // 8 * 8
+    x = x[:rows].reshape(rows // 8, 8 * block)  # 8 blocks per row
+    (res,) = gpu_codec(hl, [x], code, block)
+    check_unit(orc, x, res, code, block, what="all bf16")
+
+
+@pytest.mark.parametrize("code", [0, 1], ids=["int8", "e4m3fn"])
+def test_every_scale_mantissa(hl, orc, code):
+    """amax = m * 2^e for all 128 bf16 mantissas m and e in [-70, 127]."""
+    ms = 1.0 + np.arange(128) / 128.0
+    es = np.arange(-70, 128)
+    amax = (ms[None, :] * np.exp2(es)[:, None]).astype(np.float32).ravel()
+    amax = amax[np.isfinite(amax)]
+    block = 64
+    g = np.random.default_rng(3)
+    x = (g.uniform(-1, 1, (amax.size, block)) * amax[:, None]).astype(np.float32)
+    x[:, 5] = -amax
+    x = np.nan_to_num(x)
+    xb = wl.to_bf16_bits(x)
+    rows = xb.shape[0] // 4 * 4
+    xb = xb[:rows].reshape(rows // 4, 4 * block)
+    (res,) = gpu_codec(hl, [xb], code, block)
+    check_unit(orc, xb, res, code, block, what="scale mantissas")
+
+
+@pytest.mark.parametrize("code", [0, 1], ids=["int8", "e4m3fn"])
+def test_zero_and_tiny_blocks(hl, orc, code):
+    x = np.zeros((8, 512), dtype=np.float32)
+    x[1, 3] = 2.0 ** -65
+    x[2, 40] = -(2.0 ** -64)
+    x[3, 100:110] = -0.0
+    x[4, :] = -0.0
+    x[5, 64:128] = np.linspace(-1e-25, 1e-25, 64)
+    xb = wl.to_bf16_bits(x)
+    (res,) = gpu_codec(hl, [xb], code, 32)
+    check_unit(orc, xb, res, code, 32, what="zero blocks")
+
+
+def test_many_units_one_call(hl, orc):
+    """More units than one launch carries, with different shapes."""
+    xs = [wl.activation_host(17 + 13 * i, 128 * (1 + i % 5), seed=200 + i) for i in range(37)]
+    res = gpu_codec(hl, xs, 1, 128)
+    for i, (x, r) in enumerate(zip(xs, res)):
+        check_unit(orc, x, r, 1, 128, what=f"unit {i}")
+
+
+def test_without_stats(hl, orc):
+    x = wl.activation_host(64, 1024, seed=8)
+    (res,) = gpu_codec(hl, [x], 0, 128, stats=False)
+    check_unit(orc, x, res, 0, 128, what="no stats")
+
+
+def test_deterministic(hl, orc):
+    xs = [wl.activation_host(300, 3584, seed=9, outliers=("channels", 0.005, 30.0))]
+    r1 = gpu_codec(hl, xs, 1, 128)[0]
+    r2 = gpu_codec(hl, xs, 1, 128)[0]
+    for a, b in zip(r1, r2):
+        assert_bytes_equal(a, b, "repeat")

@@ -1,0 +1,207 @@
+"""Full-size workloads on the GPU, in the launch configuration the benchmark
+times, checked against the oracle on every row it can afford and on sampled
+rows / entries elsewhere.
+
+  - Qwen2-7B-width layer: hidden 16384x3584 and MLP 16384x18944, fp8-e4m3
+    1x128 (the hidden unit fully, the MLP unit on sampled rows);
+  - whole-model plan: 78 L units of 16384x3584, int8 1x64, one batched call;
+  - fused wgrad: X 16384x4096 fp8-e4m3 1x128, dY 16384x4096, dW 4096x4096
+    (the 512x512 corner against fp64, sampled entries, and the whole matrix
+    against an fp32 GEMM on the decompressed operand);
+  - Llama-3-8B-shaped stress: 32 MLP intermediates 32768x14336, Student-t,
+    int8 1x128 (sampled rows of every unit).
+The inputs are drawn on the device (torch's generator), then the rows the
+oracle needs are copied back, byte for byte.
+"""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_33570_amd import workloads as wl
+from gpu_util import assert_bytes_equal, assert_close, dev, filled, host, rel_fro
+
+pytestmark = [pytest.mark.gpu, pytest.mark.slow]
+
+
+@pytest.fixture(autouse=True)
+def _free():
+    yield
+    torch.cuda.synchronize()
+    torch.cuda.empty_cache()
+
+
+def bf16_rows(t, idx):
+    return host(t[torch.as_tensor(idx, device=t.device)])
+
+
+def alloc_unit(hl, x, block, stats=True):
+    rows, cols = x.shape
+    codes = torch.empty((rows, cols), dtype=torch.uint8, device="cuda")
+    scales = torch.empty((rows, cols // block), dtype=torch.float32, device="cuda")
+    xhat = torch.empty((rows, cols), dtype=torch.bfloat16, device="cuda")
+    ssx = torch.empty(rows, dtype=torch.float32, device="cuda") if stats else None
+    sse = torch.empty(rows, dtype=torch.float32, device="cuda") if stats else None
+    d_c = hl.unit_desc(x=x, codes=codes, scales=scales, row_ss_x=ssx, row_ss_err=sse)
+    d_d = hl.unit_desc(codes=codes, scales=scales, xhat=xhat)
+    return dict(x=x, codes=codes, scales=scales, xhat=xhat, ssx=ssx, sse=sse, dc=d_c, dd=d_d)
+
+
+def check_rows(orc, u, idx, code, block, what):
+    x = bf16_rows(u["x"], idx)
+    o_codes, o_scales = orc.quantize(x, code, block)
+    o_xhat = orc.dequantize(o_codes, o_scales, code, block)
+    assert_bytes_equal(host(u["codes"][torch.as_tensor(idx, device="cuda")]), o_codes, what + " codes")
+    assert_bytes_equal(host(u["scales"][torch.as_tensor(idx, device="cuda")]), o_scales,
+                       what + " scales")
+    assert_bytes_equal(bf16_rows(u["xhat"], idx), o_xhat, what + " xhat")
+    if u["ssx"] is not None:
+        o_ssx, o_sse = orc.row_stats(x, o_xhat)
+        assert_close(host(u["ssx"])[idx], o_ssx, what + " ss_x")
+        assert_close(host(u["sse"])[idx], o_sse, what + " ss_err")
+
+
+def grpo_on_gpu(hl, b):
+    R, n = b.P * b.G, b.P * b.G * b.T
+    adv = torch.empty(R, dtype=torch.float32, device="cuda")
+    flags = torch.empty(n, dtype=torch.uint8, device="cuda")
+    coeff = torch.empty(n, dtype=torch.float32, device="cuda")
+    m = dev(b.mask) if b.mask is not None else None
+    hl.hilore_grpo_coeffs(dev(b.rewards), dev(b.logp_new), dev(b.logp_old), None, m, b.P, b.G,
+                          b.T, 0.2, 1e-6, 0.0, 0.0, adv, None, flags, coeff)
+    return coeff, m
+
+
+def test_qwen2_7b_layer(hl, orc):
+    w = wl.QWEN2_7B_LAYER
+    code, block = 1, 128
+    b = wl.grpo_batch(w.P, w.G, w.T, seed=w.seed)
+    coeff, m = grpo_on_gpu(hl, b)
+    units = [alloc_unit(hl, wl.activation_device(s.rows, s.cols, w.seed * 10 + i,
+                                                 outliers=w.outliers), block)
+             for i, s in enumerate(w.units)]
+    hl.hilore_compress([u["dc"] for u in units], code, block)
+    expo = torch.empty(2, dtype=torch.float32, device="cuda")
+    risk = torch.empty_like(expo)
+    rel = torch.empty_like(expo)
+    rows = b.P * b.G * b.T
+    hl.hilore_unit_exposure_risk(coeff, m, rows, [u["dc"] for u in units], 1e-8, 1e-8, expo,
+                                 risk, rel)
+    hl.hilore_decompress([u["dd"] for u in units], code, block)
+    torch.cuda.synchronize()
+    _, _, _, o_coeff = orc.grpo_coeffs(b.rewards, b.logp_new, b.logp_old, None, None, w.P, w.G,
+                                       w.T)
+    # hidden unit: every row against the oracle, and its exposure / risk
+    hid = units[0]
+    x = host(hid["x"])
+    o_codes, o_scales = orc.quantize(x, code, block)
+    o_xhat = orc.dequantize(o_codes, o_scales, code, block)
+    assert_bytes_equal(host(hid["codes"]), o_codes, "hidden codes")
+    assert_bytes_equal(host(hid["scales"]), o_scales, "hidden scales")
+    assert_bytes_equal(host(hid["xhat"]), o_xhat, "hidden xhat")
+    o_ssx, o_sse = orc.row_stats(x, o_xhat)
+    assert_close(host(hid["ssx"]), o_ssx, "hidden ss_x")
+    assert_close(host(hid["sse"]), o_sse, "hidden ss_err")
+    e, k, r = orc.unit_exposure_risk(o_coeff, None, o_ssx, o_sse, x.shape[1])
+    assert_close(host(expo)[:1], [e], "hidden exposure")
+    assert_close(host(risk)[:1], [k], "hidden risk")
+    assert_close(host(rel)[:1], [r], "hidden rel_err")
+    # MLP unit: sampled rows; its reduction from the GPU's row sums in fp64
+    mlp = units[1]
+    idx = np.sort(np.random.default_rng(1).choice(rows, 96, replace=False))
+    check_rows(orc, mlp, idx, code, block, "mlp")
+    e, k, r = orc.unit_exposure_risk(o_coeff, None, host(mlp["ssx"]).astype(np.float64),
+                                     host(mlp["sse"]).astype(np.float64), mlp["x"].shape[1])
+    assert_close(host(expo)[1:], [e], "mlp exposure")
+    assert_close(host(risk)[1:], [k], "mlp risk")
+    assert_close(host(rel)[1:], [r], "mlp rel_err")
+
+
+def test_qwen2_7b_plan(hl, orc):
+    w = wl.QWEN2_7B_PLAN
+    code, block = 0, 64
+    act = wl.plan_actions(len(w.units), w.seed)
+    L = np.nonzero(act == "L")[0]
+    assert len(L) == 78 and (act == "H").sum() == 59 and (act == "R").sum() == 59
+    b = wl.grpo_batch(w.P, w.G, w.T, seed=w.seed)
+    coeff, m = grpo_on_gpu(hl, b)
+    rows = b.P * b.G * b.T
+    units = [alloc_unit(hl, wl.activation_device(rows, 3584, w.seed * 1000 + int(u),
+                                                 outliers=w.outliers), block) for u in L]
+    hl.hilore_compress([u["dc"] for u in units], code, block)
+    n = len(units)
+    expo = torch.empty(n, dtype=torch.float32, device="cuda")
+    risk = torch.empty_like(expo)
+    rel = torch.empty_like(expo)
+    hl.hilore_unit_exposure_risk(coeff, m, rows, [u["dc"] for u in units], 1e-8, 1e-8, expo,
+                                 risk, rel)
+    hl.hilore_decompress([u["dd"] for u in units], code, block)
+    torch.cuda.synchronize()
+    _, _, _, o_coeff = orc.grpo_coeffs(b.rewards, b.logp_new, b.logp_old, None, None, w.P, w.G,
+                                       w.T)
+    g = np.random.default_rng(2)
+    for i, u in enumerate(units):
+        check_rows(orc, u, np.sort(g.choice(rows, 6, replace=False)), code, block, f"unit {i}")
+    ge, gk, gr = host(expo), host(risk), host(rel)
+    for i in (0, n - 1):  # two units end to end against the oracle
+        x = host(units[i]["x"])
+        c, s = orc.quantize(x, code, block)
+        ssx, sse = orc.row_stats(x, orc.dequantize(c, s, code, block))
+        e, k, r = orc.unit_exposure_risk(o_coeff, None, ssx, sse, 3584)
+        assert_close([ge[i], gk[i], gr[i]], [e, k, r], f"unit {i} exposure/risk/rel")
+    for i in range(n):  # every unit's reduction from its GPU row sums
+        e, k, r = orc.unit_exposure_risk(o_coeff, None, host(units[i]["ssx"]).astype(np.float64),
+                                         host(units[i]["sse"]).astype(np.float64), 3584)
+        assert_close([ge[i], gk[i], gr[i]], [e, k, r], f"unit {i} reduction")
+    assert np.isfinite(gk.astype(np.float64).sum())
+
+
+def test_wgrad_4096(hl, orc):
+    w = wl.WGRAD_4096
+    K, M, N = w.wgrad
+    code, block = 1, 128
+    x = wl.activation_device(K, M, w.seed)
+    u = alloc_unit(hl, x, block, stats=False)
+    hl.hilore_compress([u["dc"]], code, block)
+    hl.hilore_decompress([u["dd"]], code, block)
+    dy = wl.normal_bf16_device(K, N, w.seed + 100, 0.02)
+    dw = filled((M, N), torch.float32, float("nan"))
+    hl.hilore_dequant_wgrad(u["codes"], u["scales"], code, block, dy, dw, K, M, N, False)
+    torch.cuda.synchronize()
+    check_rows(orc, u, np.sort(np.random.default_rng(3).choice(K, 64, replace=False)), code,
+               block, "X")
+    # whole matrix against an fp32 GEMM on the decompressed operand
+    ref = u["xhat"].float().t().contiguous() @ dy.float()
+    assert rel_fro(host(dw), host(ref)) <= 1e-5
+    # 512 x 512 corner against fp64
+    codes_h = host(u["codes"])
+    scales_h = host(u["scales"])
+    dy_h = host(dy)
+    c512 = np.ascontiguousarray(codes_h[:, :512])
+    s512 = np.ascontiguousarray(scales_h[:, :512 // block])
+    d512 = np.ascontiguousarray(dy_h[:, :512])
+    v0 = orc.wgrad(c512, s512, code, block, d512, variant=0)
+    v1 = orc.wgrad(c512, s512, code, block, d512, variant=1)
+    got = host(dw)[:512, :512]
+    assert rel_fro(got, v0) <= 2e-2
+    assert rel_fro(got, v1) <= 1e-5
+    # sampled entries anywhere in dW
+    g = np.random.default_rng(4)
+    ii, jj = g.integers(0, M, 64), g.integers(0, N, 64)
+    ent = orc.wgrad_entries(codes_h, scales_h, code, block, dy_h, ii, jj, variant=1)
+    assert_close(host(dw)[ii, jj], ent, "sampled dW entries", rel=1e-4)
+
+
+def test_llama3_8b_stress(hl, orc):
+    w = wl.LLAMA3_8B_STRESS
+    code, block = 0, 128
+    units = []
+    for i, s in enumerate(w.units):
+        units.append(alloc_unit(hl, wl.activation_device(s.rows, s.cols, w.seed * 100 + i,
+                                                         dist="student_t3"), block))
+    hl.hilore_compress([u["dc"] for u in units], code, block)
+    hl.hilore_decompress([u["dd"] for u in units], code, block)
+    torch.cuda.synchronize()
+    g = np.random.default_rng(5)
+    for i, u in enumerate(units):
+        check_rows(orc, u, np.sort(g.choice(w.units[0].rows, 3, replace=False)), code, block,
+                   f"layer {i}")

@@ -1,0 +1,80 @@
+"""GPU parity of hilore_unit_exposure_risk, run on the GPU's own coefficients
+and row sums, against the oracle's fp64 truth built from the same inputs."""
+import numpy as np
+import pytest
+import torch
+
+from paper_2609_33570_amd import workloads as wl
+from gpu_util import assert_close, dev, filled, host
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_pipeline(hl, b, xs, code, block, beta=0.0):
+    """GRPO coefficients, batched compress with row sums, then the per-unit
+    reduction, all on one stream, like one microbatch of the hot path."""
+    R, n = b.P * b.G, b.P * b.G * b.T
+    adv = filled(R, torch.float32, 0)
+    flags = filled(n, torch.uint8, 0)
+    coeff = filled(n, torch.float32, float("nan"))
+    m = dev(b.mask) if b.mask is not None else None
+    hl.hilore_grpo_coeffs(dev(b.rewards), dev(b.logp_new), dev(b.logp_old),
+                          dev(b.logp_ref) if b.logp_ref is not None else None, m, b.P, b.G, b.T,
+                          0.2, 1e-6, beta, 0.0, adv, None, flags, coeff)
+    units, keep = [], []
+    for x in xs:
+        rows, cols = x.shape
+        xd = dev(x)
+        codes = torch.empty((rows, cols), dtype=torch.uint8, device="cuda")
+        scales = torch.empty((rows, cols // block), dtype=torch.float32, device="cuda")
+        ssx = filled(rows, torch.float32, float("nan"))
+        sse = filled(rows, torch.float32, float("nan"))
+        keep.append((xd, codes, scales, ssx, sse))
+        units.append(hl.unit_desc(x=xd, codes=codes, scales=scales, row_ss_x=ssx, row_ss_err=sse))
+    hl.hilore_compress(units, code, block)
+    k = len(xs)
+    expo = filled(k, torch.float32, float("nan"))
+    risk = filled(k, torch.float32, float("nan"))
+    rel = filled(k, torch.float32, float("nan"))
+    hl.hilore_unit_exposure_risk(coeff, m, n, units, 1e-8, 1e-8, expo, risk, rel)
+    torch.cuda.synchronize()
+    return host(expo), host(risk), host(rel)
+
+
+def oracle_pipeline(orc, b, xs, code, block, beta=0.0):
+    _, _, _, coeff = orc.grpo_coeffs(b.rewards, b.logp_new, b.logp_old, b.logp_ref, b.mask,
+                                     b.P, b.G, b.T, beta=beta)
+    out = []
+    for x in xs:
+        codes, scales = orc.quantize(x, code, block)
+        xh = orc.dequantize(codes, scales, code, block)
+        ss_x, ss_e = orc.row_stats(x, xh)
+        out.append(orc.unit_exposure_risk(coeff, b.mask, ss_x, ss_e, x.shape[1]))
+    return [np.array(v) for v in zip(*out)]
+
+
+@pytest.mark.parametrize("code,block", [(0, 64), (1, 128)], ids=["int8-64", "e4m3fn-128"])
+@pytest.mark.parametrize("pad", [None, 0.3])
+@pytest.mark.parametrize("beta", [0.0, 1e-3])
+def test_units_of_a_microbatch(hl, orc, code, block, pad, beta):
+    b = wl.grpo_batch(2, 8, 256, seed=41, with_ref=beta > 0, pad_frac=pad, delta_sigma=0.1)
+    rows = b.P * b.G * b.T
+    xs = [wl.activation_host(rows, c, seed=300 + i, outliers=("channels", 0.005, 30.0))
+          for i, c in enumerate([256, 512, 1024, 768, 1536])]
+    g = gpu_pipeline(hl, b, xs, code, block, beta)
+    o = oracle_pipeline(orc, b, xs, code, block, beta)
+    for name, gv, ov in zip(["exposure", "risk", "rel_err"], g, o):
+        assert_close(gv, ov, name)
+
+
+def test_many_units_and_empty_token_set(hl, orc):
+    b = wl.grpo_batch(1, 8, 128, seed=42, pad_frac=0.4)
+    rows = 1024
+    xs = [wl.activation_host(rows, 128, seed=400 + i) for i in range(40)]
+    g = gpu_pipeline(hl, b, xs, 0, 64)
+    o = oracle_pipeline(orc, b, xs, 0, 64)
+    for name, gv, ov in zip(["exposure", "risk", "rel_err"], g, o):
+        assert_close(gv, ov, name)
+    b.mask[:] = 0
+    g = gpu_pipeline(hl, b, xs[:3], 0, 64)
+    assert (g[0] == 0).all() and (g[1] == 0).all() and (g[2] > 0).all()
