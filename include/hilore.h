@@ -23,7 +23,8 @@
  *     nothing is enqueued and no output is touched.  Validation touches no
  *     device state, so argument errors are reported even without a GPU.
  *   - bf16 tensors are passed as uint16_t* (raw bit patterns).
- *   - Alignment: every tensor pointer must be 16-byte aligned.
+ *   - Alignment: every tensor pointer must be 16-byte aligned, except the
+ *     per-unit outputs of hilore_unit_exposure_risk (4-byte aligned).
  *   - The functions are re-entrant; calls on different streams may run
  *     concurrently.  No C++ exception crosses this interface.
  *   - Results do not depend on the launch configuration: every reduction is

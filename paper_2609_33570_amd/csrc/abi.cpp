@@ -187,9 +187,10 @@ hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask,
   if (!units || !exposure || !risk || !rel_err) return HILORE_ERR_INVALID_ARG;
   if (rows >= (int64_t(1) << 24)) return HILORE_ERR_UNSUPPORTED;
   if (rows > 0 && !coeff) return HILORE_ERR_INVALID_ARG;
-  const void *ptrs[] = {coeff, mask, exposure, risk, rel_err};
-  for (const void *p : ptrs)
-    if (p && !aligned16(p)) return HILORE_ERR_ALIGNMENT;
+  if ((coeff && !aligned16(coeff)) || (mask && !aligned16(mask))) return HILORE_ERR_ALIGNMENT;
+  const void *outs[] = {exposure, risk, rel_err};  // written one float at a time
+  for (const void *p : outs)
+    if ((reinterpret_cast<uintptr_t>(p) & 3u) != 0) return HILORE_ERR_ALIGNMENT;
   for (int i = 0; i < n_units; ++i) {
     const hilore_unit_desc &u = units[i];
     if (u.rows != rows || u.cols <= 0) return HILORE_ERR_INVALID_ARG;

@@ -31,6 +31,10 @@
 #include "device_common.hpp"
 #include "hilore_internal.hpp"
 
+// Every rounding step is the one written: no implicit fused multiply-add
+// (the exact sequences above depend on it; wanted FMAs are explicit fmaf).
+#pragma clang fp contract(off)
+
 namespace hilore {
 namespace {
 

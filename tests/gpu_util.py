@@ -31,11 +31,15 @@ def host(t: torch.Tensor) -> np.ndarray:
 
 
 def empty(shape, dtype) -> torch.Tensor:
+    if isinstance(shape, int):
+        shape = (shape,)
     return torch.empty(shape, dtype=dtype, device="cuda")
 
 
 def filled(shape, dtype, value=0) -> torch.Tensor:
     """A buffer pre-filled with a sentinel so unwritten outputs are noticed."""
+    if isinstance(shape, int):
+        shape = (shape,)
     return torch.full(shape, value, dtype=dtype, device="cuda")
 
 

@@ -137,6 +137,7 @@ def test_exposure_risk_validation(lib):
     assert risk(lib, [ok], coeff=None) == E.HILORE_ERR_INVALID_ARG
     assert risk(lib, [ok], outs=(None, FAKE, FAKE)) == E.HILORE_ERR_INVALID_ARG
     assert risk(lib, [ok], mask=FAKE + 1) == E.HILORE_ERR_ALIGNMENT
+    assert risk(lib, [ok], outs=(FAKE, FAKE + 2, FAKE)) == E.HILORE_ERR_ALIGNMENT
     assert risk(lib, [ok], eps=(-1.0, 1e-8)) == E.HILORE_ERR_INVALID_ARG
     assert risk(lib, [unit(row_ss_x=FAKE, row_ss_err=FAKE, cols=0)]) == E.HILORE_ERR_INVALID_ARG
     assert risk(lib, []) == E.HILORE_OK
