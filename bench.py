@@ -41,7 +41,9 @@ def parse():
     p.add_argument("--steps", type=int, default=20)
     p.add_argument("--warmup", type=int, default=5)
     p.add_argument("--no-cpu-baseline", action="store_true")
-    p.add_argument("--cpu-rows", type=int, default=1024,
+    p.add_argument("--copy-calibration", action="store_true",
+                   help="also run a plain 1 GiB device copy (for scaling HBM byte counters)")
+    p.add_argument("--cpu-rows", type=int, default=8192,
                    help="MLP rows (and 4x as many hidden rows) in the oracle's timed sample")
     return p.parse_args()
 
@@ -151,6 +153,14 @@ def main():
                                 False)
         mark(5)
 
+    if args.copy_calibration:
+        # a plain copy of known size: 2^29 bf16 = 1 GiB read + 1 GiB written
+        src = torch.ones(1 << 29, dtype=torch.bfloat16, device="cuda")
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        del src, dst
     progress("warm-up")
     for i in range(args.warmup):
         step(sets[i % N_SETS])

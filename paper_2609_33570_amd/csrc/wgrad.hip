@@ -81,29 +81,56 @@ struct LoadPlan {
   uint32_t st_x, st_s, st_y;  // byte stride of one token row
 };
 
+// Buffer descriptors of one stage of 64 token rows starting at k0.  Past
+// the end of K the range is empty and every load returns 0.
+struct StageRsrc {
+  __amdgpu_buffer_rsrc_t x, s, y;
+};
+
 template <int BLOCK>
-__device__ __forceinline__ void load_stage(Stage &st, const LoadPlan &lp, const WgradArgs &a,
-                                           int64_t k0) {
+__device__ __forceinline__ StageRsrc stage_rsrc(const WgradArgs &a, int64_t k0) {
   const int64_t left = a.K - k0;
-  const int64_t rows = left < BK ? left : BK;
+  const int64_t rows = left <= 0 ? 0 : (left < BK ? left : BK);
   const int64_t sld = a.M / BLOCK;
-  const __amdgpu_buffer_rsrc_t rx = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)(a.codes + k0 * a.M), 0, (int)(rows * a.M), 0x00020000);
-  const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)(a.scales + k0 * sld), 0, (int)(rows * sld * 4), 0x00020000);
-  const __amdgpu_buffer_rsrc_t ry = __builtin_amdgcn_make_buffer_rsrc(
-      (void *)(a.dy + k0 * a.N), 0, (int)(rows * a.N * 2), 0x00020000);
+  StageRsrc r;
+  r.x = __builtin_amdgcn_make_buffer_rsrc((void *)(a.codes + k0 * a.M), 0, (int)(rows * a.M),
+                                          0x00020000);
+  r.s = __builtin_amdgcn_make_buffer_rsrc((void *)(a.scales + k0 * sld), 0,
+                                          (int)(rows * sld * 4), 0x00020000);
+  r.y = __builtin_amdgcn_make_buffer_rsrc((void *)(a.dy + k0 * a.N), 0, (int)(rows * a.N * 2),
+                                          0x00020000);
+  return r;
+}
+
+// Token rows R0, R0+1 of this thread's 8-row patch (6 loads).
+template <int R0>
+__device__ __forceinline__ void load_rows(Stage &st, const StageRsrc &rs, const LoadPlan &lp) {
 #pragma unroll
-  for (int r = 0; r < 8; ++r) {
-    st.xc[r] = __builtin_amdgcn_raw_buffer_load_b64(rx, (int)(lp.vo_x + r * lp.st_x), 0, 0);
+  for (int r = R0; r < R0 + 2; ++r) {
+    st.xc[r] = __builtin_amdgcn_raw_buffer_load_b64(rs.x, (int)(lp.vo_x + r * lp.st_x), 0, 0);
     st.xs[r] = __uint_as_float(
-        __builtin_amdgcn_raw_buffer_load_b32(rs, (int)(lp.vo_s + r * lp.st_s), 0, 0));
-    st.yv[r] = __builtin_amdgcn_raw_buffer_load_b128(ry, (int)(lp.vo_y + r * lp.st_y), 0, 0);
+        __builtin_amdgcn_raw_buffer_load_b32(rs.s, (int)(lp.vo_s + r * lp.st_s), 0, 0));
+    st.yv[r] = __builtin_amdgcn_raw_buffer_load_b128(rs.y, (int)(lp.vo_y + r * lp.st_y), 0, 0);
   }
 }
 
-template <int CODE, int C>
-__device__ __forceinline__ void store_x_pair(const Stage &st, uint8_t *a_lds, int lc, int g) {
+template <int BLOCK>
+__device__ __forceinline__ void load_stage(Stage &st, const LoadPlan &lp, const WgradArgs &a,
+                                           int64_t k0) {
+  const StageRsrc rs = stage_rsrc<BLOCK>(a, k0);
+  load_rows<0>(st, rs, lp);
+  load_rows<2>(st, rs, lp);
+  load_rows<4>(st, rs, lp);
+  load_rows<6>(st, rs, lp);
+}
+
+// Quarter Q of a stage's LDS fill: X columns 2Q, 2Q+1 dequantised and dY
+// columns 2Q, 2Q+1, each written as one t-contiguous 16-byte granule per
+// column (rows (t, t+1) paired into one word).
+template <int CODE, int Q>
+__device__ __forceinline__ void store_quarter(const Stage &st, uint8_t *a_lds, uint8_t *b_lds,
+                                              int lc, int g) {
+  constexpr int C = 2 * Q;
   float lo[8], hi[8];
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
@@ -122,31 +149,105 @@ __device__ __forceinline__ void store_x_pair(const Stage &st, uint8_t *a_lds, in
   p.z = pack_bf16(hi[4], hi[5]);
   p.w = pack_bf16(hi[6], hi[7]);
   *reinterpret_cast<u32x4 *>(a_lds + lds_off(lc * 8 + C + 1, g)) = p;
+#pragma unroll
+  for (int c = C; c < C + 2; ++c) {
+    const uint32_t sel = (c & 1) ? 0x07060302u : 0x05040100u;
+    p.x = __builtin_amdgcn_perm(st.yv[1][Q], st.yv[0][Q], sel);
+    p.y = __builtin_amdgcn_perm(st.yv[3][Q], st.yv[2][Q], sel);
+    p.z = __builtin_amdgcn_perm(st.yv[5][Q], st.yv[4][Q], sel);
+    p.w = __builtin_amdgcn_perm(st.yv[7][Q], st.yv[6][Q], sel);
+    *reinterpret_cast<u32x4 *>(b_lds + lds_off(lc * 8 + c, g)) = p;
+  }
 }
 
 template <int CODE>
 __device__ __forceinline__ void store_stage(const Stage &st, uint8_t *a_lds, uint8_t *b_lds,
                                             int tid) {
-  const int lc = tid & 31;
-  const int g = tid >> 5;  // granule = kg / 8
-  // X: dequantise two columns of the 8 token rows at a time and pair rows
-  // (t, t+1) of each column into one word.
-  store_x_pair<CODE, 0>(st, a_lds, lc, g);
-  store_x_pair<CODE, 2>(st, a_lds, lc, g);
-  store_x_pair<CODE, 4>(st, a_lds, lc, g);
-  store_x_pair<CODE, 6>(st, a_lds, lc, g);
-  // dY: pair the bf16 of rows (t, t+1) for each column.
+  const int lc = tid & 31, g = tid >> 5;
+  store_quarter<CODE, 0>(st, a_lds, b_lds, lc, g);
+  store_quarter<CODE, 1>(st, a_lds, b_lds, lc, g);
+  store_quarter<CODE, 2>(st, a_lds, b_lds, lc, g);
+  store_quarter<CODE, 3>(st, a_lds, b_lds, lc, g);
+}
+
+struct Frags {
+  bf16x8 a[4], b[4];
+};
+
+// MFMA operands of k-step KS (t = 16 KS .. 16 KS + 15) for this wave.
+template <int KS>
+__device__ __forceinline__ void read_frags(Frags &f, const uint8_t *al, int wm, int wn, int lrow,
+                                           int lk) {
+  const uint8_t *bl = al + kTileBytes;
 #pragma unroll
-  for (int c = 0; c < 8; ++c) {
-    const int w = c >> 1;
-    const uint32_t sel = (c & 1) ? 0x07060302u : 0x05040100u;
-    u32x4 p;
-    p.x = __builtin_amdgcn_perm(st.yv[1][w], st.yv[0][w], sel);
-    p.y = __builtin_amdgcn_perm(st.yv[3][w], st.yv[2][w], sel);
-    p.z = __builtin_amdgcn_perm(st.yv[5][w], st.yv[4][w], sel);
-    p.w = __builtin_amdgcn_perm(st.yv[7][w], st.yv[6][w], sel);
-    *reinterpret_cast<u32x4 *>(b_lds + lds_off(lc * 8 + c, g)) = p;
+  for (int i = 0; i < 4; ++i) {
+    f.a[i] = *reinterpret_cast<const bf16x8 *>(al + lds_off(wm * 128 + i * 32 + lrow, KS * 2 + lk));
+    f.b[i] = *reinterpret_cast<const bf16x8 *>(bl + lds_off(wn * 128 + i * 32 + lrow, KS * 2 + lk));
   }
+}
+
+__device__ __forceinline__ void mma16(f32x16 (&acc)[4][4], const Frags &f) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i)
+#pragma unroll
+    for (int j = 0; j < 4; ++j)
+      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
+}
+
+// Instruction order of one k-step region: the LDS reads of the next
+// k-step's fragments first (they have all 16 MFMAs to land), then every MFMA
+// followed by three VALU ops of the next stage's dequantisation, with that
+// quarter's four LDS stores and six global loads spread between the MFMAs.
+template <bool PREFETCH, bool LOADS>
+__device__ __forceinline__ void schedule_region() {
+  if constexpr (PREFETCH) __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // 8 LDS reads
+#pragma unroll
+  for (int i = 0; i < 16; ++i) {
+    __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);                  // 1 MFMA
+    __builtin_amdgcn_sched_group_barrier(0x002, 3, 0);                  // 3 VALU
+    if (i % 4 == 3) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);  // 1 LDS write
+    if (LOADS && i < 8) __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);  // global loads
+    if (LOADS && i >= 8) __builtin_amdgcn_sched_group_barrier(0x020, 1, 0);
+  }
+  __builtin_amdgcn_sched_barrier(0);
+}
+
+// One k-step region of a stage: MFMAs of k-step KS from the current buffer
+// and quarter KS of the next stage's LDS fill.  The first region also issues
+// every global load of the stage after that: each LDS fill quarter needs all
+// eight token rows of its patch, so the loads get a whole stage to land.
+template <int CODE, int KS>
+__device__ __forceinline__ void region(f32x16 (&acc)[4][4], Frags (&f)[2], const uint8_t *cur,
+                                       uint8_t *nxt, const Stage &fill, Stage &load,
+                                       const StageRsrc &rs, const LoadPlan &lp, int wm, int wn,
+                                       int lrow, int lk, int lc, int g) {
+  if constexpr (KS < 3) read_frags<KS + 1>(f[(KS + 1) & 1], cur, wm, wn, lrow, lk);
+  if constexpr (KS == 0) {
+    load_rows<0>(load, rs, lp);
+    load_rows<2>(load, rs, lp);
+    load_rows<4>(load, rs, lp);
+    load_rows<6>(load, rs, lp);
+  }
+  store_quarter<CODE, KS>(fill, nxt, nxt + kTileBytes, lc, g);
+  mma16(acc, f[KS & 1]);
+  schedule_region<(KS < 3), (KS == 0)>();
+}
+
+// A full stage: MFMAs on `cur`, the LDS fill of the next stage from `fill`
+// into `nxt`, the loads of the stage after that into `load`.
+template <int CODE, int BLOCK>
+__device__ __forceinline__ void stage(f32x16 (&acc)[4][4], const uint8_t *cur, uint8_t *nxt,
+                                      const Stage &fill, Stage &load, const WgradArgs &a,
+                                      int64_t k_load, const LoadPlan &lp, int wm, int wn,
+                                      int lrow, int lk, int lc, int g) {
+  const StageRsrc rs = stage_rsrc<BLOCK>(a, k_load);
+  Frags f[2];
+  read_frags<0>(f[0], cur, wm, wn, lrow, lk);
+  region<CODE, 0>(acc, f, cur, nxt, fill, load, rs, lp, wm, wn, lrow, lk, lc, g);
+  region<CODE, 1>(acc, f, cur, nxt, fill, load, rs, lp, wm, wn, lrow, lk, lc, g);
+  region<CODE, 2>(acc, f, cur, nxt, fill, load, rs, lp, wm, wn, lrow, lk, lc, g);
+  region<CODE, 3>(acc, f, cur, nxt, fill, load, rs, lp, wm, wn, lrow, lk, lc, g);
+  __syncthreads();
 }
 
 template <int CODE, int BLOCK>
@@ -171,11 +272,11 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_kernel(const WgradArgs a, i
   const int lane = tid & 63;
   const int wm = wave >> 1, wn = wave & 1;
   const int lrow = lane & 31, lk = lane >> 5;
+  const int lc = tid & 31, g = tid >> 5;
 
   LoadPlan lp;
   {
-    const int lc = tid & 31;
-    const uint32_t kg = (uint32_t)(tid >> 5) * 8u;
+    const uint32_t kg = (uint32_t)g * 8u;
     const int64_t m = m0 + lc * 8, n = n0 + lc * 8;
     lp.st_x = (uint32_t)a.M;
     lp.st_s = (uint32_t)(a.M / BLOCK) * 4u;
@@ -191,40 +292,29 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_kernel(const WgradArgs a, i
 #pragma unroll
     for (int j = 0; j < 4; ++j) acc[i][j] = f32x16{};
 
-  const int64_t n_stages = (a.K + BK - 1) / BK;
-  Stage st;
-  if (n_stages > 0) {
-    load_stage<BLOCK>(st, lp, a, 0);
-    store_stage<CODE>(st, lds, lds + kTileBytes, tid);
-  }
+  // Pipeline.  Stage s of 64 tokens lives in LDS buffer s % 2; the raw
+  // (undequantised) operands of stage s+1 wait in registers.  Stage s
+  //   - runs its 64 MFMAs from LDS, four k-step regions of 16,
+  //   - dequantises and transposes stage s+1 into the other LDS buffer, a
+  //     quarter per region, interleaved with the MFMAs,
+  //   - issues the global loads of stage s+2 into the register set that
+  //     held stage s, a quarter per region,
+  //   - ends with one barrier.
+  // Loads of stages past K read nothing (empty buffer range) and return 0,
+  // so the loop needs no edge branches; the stage count is rounded up to
+  // even so that the buffer of every stage is a compile-time constant.
+  const int64_t n_stages = ((a.K + BK - 1) / BK + 1) & ~int64_t(1);
+  Stage ra, rb;
+  load_stage<BLOCK>(ra, lp, a, 0);
+  load_stage<BLOCK>(rb, lp, a, BK);
+  store_stage<CODE>(ra, lds, lds + kTileBytes, tid);
   __syncthreads();
 
-  for (int64_t s = 0; s < n_stages; ++s) {
-    const int cur = (int)(s & 1);
-    const bool more = s + 1 < n_stages;
-    if (more) load_stage<BLOCK>(st, lp, a, (s + 1) * BK);
-    const uint8_t *al = lds + 2 * cur * kTileBytes;
-    const uint8_t *bl = al + kTileBytes;
-#pragma unroll
-    for (int ks = 0; ks < BK / 16; ++ks) {
-      bf16x8 af[4], bf[4];
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-        af[i] = *reinterpret_cast<const bf16x8 *>(al + lds_off(wm * 128 + i * 32 + lrow, ks * 2 + lk));
-#pragma unroll
-      for (int j = 0; j < 4; ++j)
-        bf[j] = *reinterpret_cast<const bf16x8 *>(bl + lds_off(wn * 128 + j * 32 + lrow, ks * 2 + lk));
-#pragma unroll
-      for (int i = 0; i < 4; ++i)
-#pragma unroll
-        for (int j = 0; j < 4; ++j)
-          acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(af[i], bf[j], acc[i][j], 0, 0, 0);
-    }
-    if (more) {
-      uint8_t *an = lds + 2 * (cur ^ 1) * kTileBytes;
-      store_stage<CODE>(st, an, an + kTileBytes, tid);
-    }
-    __syncthreads();
+  uint8_t *const buf0 = lds;
+  uint8_t *const buf1 = lds + 2 * kTileBytes;
+  for (int64_t s = 0; s < n_stages; s += 2) {
+    stage<CODE, BLOCK>(acc, buf0, buf1, rb, ra, a, (s + 2) * BK, lp, wm, wn, lrow, lk, lc, g);
+    stage<CODE, BLOCK>(acc, buf1, buf0, ra, rb, a, (s + 3) * BK, lp, wm, wn, lrow, lk, lc, g);
   }
 
   // Epilogue.  32x32 accumulator layout: lane l holds column l % 32 and, for
