@@ -59,6 +59,29 @@ def codec_bytes(rows, cols, block, stats):
     return comp, decomp
 
 
+def measured_traffic():
+    """HBM bytes per launch from the committed rocprofv3 counter summary, for
+    the kernels whose sources are unchanged since the counters were taken."""
+    import hashlib
+
+    path = os.path.join(ROOT, "profiles", "hbm_traffic.json")
+    if not os.path.exists(path):
+        return {}
+    table = json.load(open(path))
+    csrc = os.path.join(ROOT, "paper_2609_33570_amd", "csrc")
+    common = ["device_common.hpp", "hilore_internal.hpp"]
+    files = {"compress": ["codec.hip"], "decompress": ["codec.hip"], "dequant_wgrad": ["wgrad.hip"],
+             "grpo_coeffs": ["grpo.hip"], "exposure_risk": ["risk.hip"]}
+    out = {}
+    for k, ent in table.get("kernels", {}).items():
+        h = hashlib.sha256()
+        for f in files.get(k, []) + common:
+            with open(os.path.join(csrc, f), "rb") as fh:
+                h.update(fh.read())
+        out[k] = ent["traffic_bytes"] if h.hexdigest() == ent["source_sha256"] else None
+    return out
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -193,9 +216,11 @@ def main():
     grpo_bytes = rows * (4 + 4 + 4 + 4 + 1) + R * 8
     risk_bytes = rows * (4 + 4) * len(w.units) + rows * 4
 
+    traffic = measured_traffic()
+
     def roof(name, achieved, peak, unit, bound, per_unit):
         return {"kernel": name, "bound": bound, "achieved": round(achieved, 2), "peak": peak,
-                "unit": unit, "frac": round(achieved / peak, 4), "traffic": None,
+                "unit": unit, "frac": round(achieved / peak, 4), "traffic": traffic.get(name),
                 "algorithmic": per_unit}
 
     roofs = {
@@ -257,7 +282,8 @@ def cpu_baseline(args, st, w, block, code):
     import oracle
 
     oracle.lib()
-    n_mlp, n_hid = args.cpu_rows, 4 * args.cpu_rows
+    n_mlp = min(args.cpu_rows, st["keep"][1][0].shape[0])
+    n_hid = min(4 * args.cpu_rows, st["keep"][0][0].shape[0])
     xs = [st["keep"][0][0][:n_hid], st["keep"][1][0][:n_mlp]]
     xs = [x.cpu().contiguous().view(torch.int16).numpy().view(np.uint16) for x in xs]
     total = 0
