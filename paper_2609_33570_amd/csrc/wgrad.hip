@@ -11,24 +11,31 @@
 // per SIMD: while one waits on LDS or memory or runs its dequantisation, the
 // other keeps the matrix core busy.  The contraction runs over tokens t in
 // stages of 64.  Both operands arrive token-major (t is the slow index of X
-// and dY) while MFMA wants 8 consecutive t per lane, so every thread loads an
-// 8(t) x 4(column) patch with row loads (a wave covers one full 256-column
-// row of the tile per load), transposes it in registers and writes 16-byte,
-// t-contiguous granules to LDS:
-//   - X: the dequantisation produces fp32 values anyway, and
-//     v_cvt_pk_bf16_f32 packs any two of them, so pairing (t, t+1) is free;
-//   - dY: one v_perm_b32 per output word pairs the bf16 halves of two rows.
-// LDS holds [256 rows][64 t] bf16 per operand (32 KB), double buffered
-// (128 KB of the 160 KB), with the 16-byte granule index XOR-swizzled by
-// (row ^ row/8): conflict-free both for the transposing writes (8 lanes
-// write rows 4 apart) and for the MFMA fragment reads (consecutive rows).
+// and dY) while MFMA wants 8 consecutive t per lane:
+//   - X: every thread loads an 8(t) x 4(column) patch of codes with row loads
+//     (a wave covers one full 256-column row of the tile per load),
+//     dequantises it and writes 16-byte, t-contiguous bf16 granules to LDS;
+//     v_cvt_pk_bf16_f32 packs any two fp32 values, so pairing (t, t+1) in the
+//     pack is free.  [256 rows][64 t] bf16, granule index XOR-swizzled by
+//     (row ^ row/8): conflict-free both for these writes (8 lanes write rows
+//     4 apart) and for the fragment reads (consecutive rows).
+//   - dY: copied unchanged from memory to LDS by the buffer unit (16-byte
+//     LDS-DMA loads, no registers, no LDS store instructions) as [64 t][256
+//     columns] bf16 rows, 16-byte chunk index XOR-swizzled by t.  The B
+//     fragments are read back with the transposing ds_read_b64_tr_b16: in
+//     each group of 16 lanes, lane 4a + c receives element c of the 8-byte
+//     pieces addressed by lanes a, a + 4, a + 8, a + 12, so pointing those
+//     lanes at rows t..t+3 of a 4-column slice hands every lane one column
+//     with 4 consecutive t; two such reads make a fragment.
+// Per stage LDS holds 32 KB of each operand; two stages in flight (128 KB of
+// the 160 KB).
 //
-// Pipeline per stage s (four k-step regions of 8 MFMAs per wave): every
-// region reads the next k-step's fragments after its MFMAs; regions 2 and 3
-// dequantise / transpose stage s+1 (already in registers) into the other LDS
-// buffer, then region 3 issues the global loads of stage s+2 into the same
-// registers; one barrier ends the stage.  One register set of raw operands
-// keeps the kernel at two waves per SIMD.
+// Pipeline per stage s (four k-step regions of 8 MFMAs per wave): region 0
+// starts the DMA of stage s+1's dY into the other buffer; regions 2 and 3
+// dequantise stage s+1's X (already in registers) into that buffer, and
+// region 3 then issues the global loads of stage s+2's X into the same
+// registers.  Every region reads the next k-step's fragments after its
+// MFMAs.  A wait for this thread's DMA and one barrier end the stage.
 //
 // Work distribution: workgroups are dealt round-robin to the 8 XCDs; the
 // launch index is remapped so that each XCD receives a contiguous run of
@@ -59,52 +66,81 @@ __device__ __forceinline__ uint32_t lds_off(int r, int g) {
 
 constexpr uint32_t kOob = 0x80000000u;  // a buffer offset past every range: loads 0
 
-// Raw operands of one stage for one thread: token rows kg..kg+7 (kg = 8 g) of
-// columns 4 c .. 4 c + 3 of the tile.
+// Raw X operand of one stage for one thread: token rows kg..kg+7 (kg = 8 g)
+// of columns 4 c .. 4 c + 3 of the tile.
 struct Stage {
-  uint32_t xc[8];  // X codes, 4 bytes per row
+  uint32_t xc[8];  // codes, 4 bytes per row
   float xs[8];     // the scale of each row's block
-  u32x2 yv[8];     // dY, 4 bf16 per row
 };
+
+// dY in LDS: row t of a stage at t * 512 bytes; 16-byte chunk c (columns
+// 8c .. 8c+7) stored at chunk position c ^ y_swz(t).  Rows t..t+3 of one
+// transposing read then fall in distinct banks, as do the two 16-lane
+// groups of a half-wave and the two half-waves.
+__device__ __forceinline__ uint32_t y_swz(uint32_t t) {
+  return ((t & 3u) << 2) | (((t >> 3) & 1u) << 4);
+}
 
 // Per-thread, loop-invariant parts of the stage loads.  Rows past K and
 // columns past M (N) fall outside the buffer range of the stage and read as
 // 0, so ragged edges need no branches.
 struct LoadPlan {
-  uint32_t vo_x, vo_s, vo_y;  // byte offsets of row kg inside a stage
-  uint32_t st_x, st_s, st_y;  // byte stride of one token row
+  uint32_t vo_x, vo_s;  // byte offsets of row kg inside a stage
+  uint32_t st_x, st_s;  // byte stride of one token row
+  uint32_t vo_y[4];     // dY chunk fetched by this lane in each of its 4 DMA loads
 };
 
 // Buffer descriptors of one stage of 64 token rows starting at k0.  Past
 // the end of K the range is empty and every load returns 0.
-struct StageRsrc {
-  __amdgpu_buffer_rsrc_t x, s, y;
+struct XRsrc {
+  __amdgpu_buffer_rsrc_t x, s;
 };
 
-template <int BLOCK>
-__device__ __forceinline__ StageRsrc stage_rsrc(const WgradArgs &a, int64_t k0) {
+__device__ __forceinline__ int64_t stage_rows(const WgradArgs &a, int64_t k0) {
   const int64_t left = a.K - k0;
-  const int64_t rows = left <= 0 ? 0 : (left < BK ? left : BK);
+  return left <= 0 ? 0 : (left < BK ? left : BK);
+}
+
+template <int BLOCK>
+__device__ __forceinline__ XRsrc x_rsrc(const WgradArgs &a, int64_t k0) {
+  const int64_t rows = stage_rows(a, k0);
   const int64_t sld = a.M / BLOCK;
-  StageRsrc r;
+  XRsrc r;
   r.x = __builtin_amdgcn_make_buffer_rsrc((void *)(a.codes + k0 * a.M), 0, (int)(rows * a.M),
                                           0x00020000);
   r.s = __builtin_amdgcn_make_buffer_rsrc((void *)(a.scales + k0 * sld), 0,
                                           (int)(rows * sld * 4), 0x00020000);
-  r.y = __builtin_amdgcn_make_buffer_rsrc((void *)(a.dy + k0 * a.N), 0, (int)(rows * a.N * 2),
-                                          0x00020000);
   return r;
 }
 
-__device__ __forceinline__ void load_stage(Stage &st, const StageRsrc &rs, const LoadPlan &lp) {
+__device__ __forceinline__ __amdgpu_buffer_rsrc_t y_rsrc(const WgradArgs &a, int64_t k0) {
+  const int64_t rows = stage_rows(a, k0);
+  return __builtin_amdgcn_make_buffer_rsrc((void *)(a.dy + k0 * a.N), 0, (int)(rows * a.N * 2),
+                                           0x00020000);
+}
+
+__device__ __forceinline__ void load_stage(Stage &st, const XRsrc &rs, const LoadPlan &lp) {
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
     st.xc[r] = __builtin_amdgcn_raw_buffer_load_b32(rs.x, (int)(lp.vo_x + r * lp.st_x), 0, 0);
     st.xs[r] = __uint_as_float(
         __builtin_amdgcn_raw_buffer_load_b32(rs.s, (int)(lp.vo_s + r * lp.st_s), 0, 0));
-    st.yv[r] = __builtin_amdgcn_raw_buffer_load_b64(rs.y, (int)(lp.vo_y + r * lp.st_y), 0, 0);
   }
 }
+constexpr int kXLoads = 16;  // VMEM instructions issued by load_stage
+
+typedef __attribute__((address_space(3))) void lds_void;
+
+// Stage dY rows 8 w .. 8 w + 7 into b_lds by LDS-DMA: load r of wave w
+// writes rows 8 w + 2 r and 8 w + 2 r + 1, lane l to byte 16 l of them.
+__device__ __forceinline__ void dma_dy(__amdgpu_buffer_rsrc_t rs, const LoadPlan &lp,
+                                       uint8_t *b_lds, int wave) {
+#pragma unroll
+  for (int r = 0; r < 4; ++r)
+    __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_void *)(b_lds + (wave * 8 + 2 * r) * 512),
+                                             16, (int)lp.vo_y[r], 0, 0, 0);
+}
+constexpr int kYLoads = 4;
 
 // Code bytes C, C+1 (C even) of a 4-byte word -> exact fp32 code values.
 template <int CODE, int C>
@@ -141,46 +177,38 @@ __device__ __forceinline__ void fill_x(const Stage &st, uint8_t *a_lds, int lc, 
   *reinterpret_cast<u32x4 *>(a_lds + lds_off(lc * 4 + C + 1, g)) = p;
 }
 
-// dY columns C, C+1: pair the bf16 of rows (t, t+1) of each column.
-template <int C>
-__device__ __forceinline__ void fill_y(const Stage &st, uint8_t *b_lds, int lc, int g) {
-#pragma unroll
-  for (int c = C; c < C + 2; ++c) {
-    const uint32_t sel = (c & 1) ? 0x07060302u : 0x05040100u;
-    const int w = c >> 1;
-    u32x4 p;
-    p.x = __builtin_amdgcn_perm(st.yv[1][w], st.yv[0][w], sel);
-    p.y = __builtin_amdgcn_perm(st.yv[3][w], st.yv[2][w], sel);
-    p.z = __builtin_amdgcn_perm(st.yv[5][w], st.yv[4][w], sel);
-    p.w = __builtin_amdgcn_perm(st.yv[7][w], st.yv[6][w], sel);
-    *reinterpret_cast<u32x4 *>(b_lds + lds_off(lc * 4 + c, g)) = p;
-  }
-}
-
-// Quarter Q of a stage's LDS fill (Q = 0..3: X columns 0-1, X 2-3, dY 0-1, dY 2-3).
-template <int CODE, int Q>
-__device__ __forceinline__ void fill_quarter(const Stage &st, uint8_t *lds_a, int lc, int g) {
-  if constexpr (Q == 0) fill_x<CODE, 0>(st, lds_a, lc, g);
-  if constexpr (Q == 1) fill_x<CODE, 2>(st, lds_a, lc, g);
-  if constexpr (Q == 2) fill_y<0>(st, lds_a + kTileBytes, lc, g);
-  if constexpr (Q == 3) fill_y<2>(st, lds_a + kTileBytes, lc, g);
-}
-
 struct Frags {
   bf16x8 a[4], b[2];
 };
 
+typedef short s16x4 __attribute__((ext_vector_type(4)));
+
+__device__ __forceinline__ s16x4 read_tr16(const uint8_t *p) {
+  return __builtin_amdgcn_ds_read_tr16_b64_v4i16((__attribute__((address_space(3))) s16x4 *)p);
+}
+
+// Lane-dependent LDS offsets of the fragment reads: A row wm * 128 + lrow,
+// and for B block j the transposing-read address at t = 0 (rows 16 KS and
+// 16 KS + 4 follow as constant offsets).
+struct FragPlan {
+  int wm, lrow, lk;
+  uint32_t yb[2];
+};
+
 // MFMA operands of k-step KS (t = 16 KS .. 16 KS + 15) for this wave.
 template <int KS>
-__device__ __forceinline__ void read_frags(Frags &f, const uint8_t *al, int wm, int wn, int lrow,
-                                           int lk) {
-  const uint8_t *bl = al + kTileBytes;
+__device__ __forceinline__ void read_frags(Frags &f, const uint8_t *al, const uint8_t *bl,
+                                           const FragPlan &fp) {
 #pragma unroll
   for (int i = 0; i < 4; ++i)
-    f.a[i] = *reinterpret_cast<const bf16x8 *>(al + lds_off(wm * 128 + i * 32 + lrow, KS * 2 + lk));
+    f.a[i] = *reinterpret_cast<const bf16x8 *>(
+        al + lds_off(fp.wm * 128 + i * 32 + fp.lrow, KS * 2 + fp.lk));
 #pragma unroll
-  for (int j = 0; j < 2; ++j)
-    f.b[j] = *reinterpret_cast<const bf16x8 *>(bl + lds_off(wn * 64 + j * 32 + lrow, KS * 2 + lk));
+  for (int j = 0; j < 2; ++j) {
+    const s16x4 lo = read_tr16(bl + fp.yb[j] + KS * 16 * 512);
+    const s16x4 hi = read_tr16(bl + fp.yb[j] + (KS * 16 + 4) * 512);
+    f.b[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  }
 }
 
 __device__ __forceinline__ void mma8(f32x16 (&acc)[4][2], const Frags &f) {
@@ -191,10 +219,10 @@ __device__ __forceinline__ void mma8(f32x16 (&acc)[4][2], const Frags &f) {
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
 }
 
-// Instruction order of one k-step region: every MFMA followed by a few VALU
-// ops (the next stage's dequantisation / transposition in the last two
-// regions) with that region's LDS stores and global loads spread between,
-// then the LDS reads of the next k-step's fragments.
+// Instruction order of one k-step region: every MFMA followed by VALU ops
+// of the next stage's dequantisation (last two regions), LDS stores spread
+// over the region, global loads after the first MFMAs, then the LDS reads of
+// the next k-step's fragments.
 template <bool NEXT, int VALU, int WRITES, int LOADS>
 __device__ __forceinline__ void schedule_region() {
 #pragma unroll
@@ -203,70 +231,80 @@ __device__ __forceinline__ void schedule_region() {
     if constexpr (VALU > 0) __builtin_amdgcn_sched_group_barrier(0x002, VALU, 0);
     if constexpr (WRITES > 0)
       if (i % (8 / WRITES) == 8 / WRITES - 1) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
-    if constexpr (LOADS > 0) __builtin_amdgcn_sched_group_barrier(0x020, LOADS, 0);
+    if constexpr (LOADS > 0)
+      if (i < (LOADS + 1) / 2) __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
   }
-  if constexpr (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, 6, 0);  // 6 LDS reads
+  if constexpr (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // 8 LDS reads
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// One k-step region of a stage.  Regions 0 and 1 only multiply; region 2
-// dequantises the next stage's X patch into the other LDS buffer; region 3
-// transposes its dY patch there and then issues the global loads of the
-// stage after that into the same registers (so one register set suffices and
-// the loads have until region 2 of the next stage to land).  The fragments
-// of the next k-step are read into the same registers once this k-step's
-// MFMAs have been issued; the other wave on the SIMD covers that latency.
+// One k-step region of a stage.  Region 0 starts the DMA of the next
+// stage's dY; regions 2 and 3 dequantise the next stage's X into the other
+// LDS buffer, and region 3 then issues the global loads of the stage after
+// that into the same registers (so one register set suffices and the loads
+// have until region 2 of the next stage to land).  The fragments of the next
+// k-step are read into the same registers once this k-step's MFMAs have been
+// issued; the other wave on the SIMD covers that latency.
 template <int CODE, int KS>
-__device__ __forceinline__ void region(f32x16 (&acc)[4][2], Frags &f, const uint8_t *cur,
-                                       uint8_t *nxt, Stage &raw, const StageRsrc &rs,
-                                       const LoadPlan &lp, int wm, int wn, int lrow, int lk,
-                                       int lc, int g) {
-  if constexpr (KS == 2) {
-    fill_quarter<CODE, 0>(raw, nxt, lc, g);
-    fill_quarter<CODE, 1>(raw, nxt, lc, g);
-  }
+__device__ __forceinline__ void region(f32x16 (&acc)[4][2], Frags &f, const uint8_t *cur_a,
+                                       const uint8_t *cur_b, uint8_t *nxt_a, uint8_t *nxt_b,
+                                       Stage &raw, __amdgpu_buffer_rsrc_t ry, const XRsrc &rx,
+                                       const LoadPlan &lp, const FragPlan &fp, int wave, int lc,
+                                       int g) {
+  if constexpr (KS == 0) dma_dy(ry, lp, nxt_b, wave);
+  if constexpr (KS == 2) fill_x<CODE, 0>(raw, nxt_a, lc, g);
   if constexpr (KS == 3) {
-    fill_quarter<CODE, 2>(raw, nxt, lc, g);
-    fill_quarter<CODE, 3>(raw, nxt, lc, g);
-    load_stage(raw, rs, lp);
+    fill_x<CODE, 2>(raw, nxt_a, lc, g);
+    load_stage(raw, rx, lp);
   }
   mma8(acc, f);
-  if constexpr (KS < 3) read_frags<KS + 1>(f, cur, wm, wn, lrow, lk);
-  if constexpr (KS < 2) schedule_region<true, 0, 0, 0>();
-  if constexpr (KS == 2) schedule_region<true, 8, 4, 0>();
-  if constexpr (KS == 3) schedule_region<false, 2, 4, 3>();
+  if constexpr (KS < 3) read_frags<KS + 1>(f, cur_a, cur_b, fp);
+  if constexpr (KS == 0) schedule_region<true, 0, 0, kYLoads>();
+  if constexpr (KS == 1) schedule_region<true, 0, 0, 0>();
+  if constexpr (KS == 2) schedule_region<true, 4, 2, 0>();
+  if constexpr (KS == 3) schedule_region<false, 4, 2, kXLoads>();
 }
 
-// A full stage: MFMAs on `cur`, the LDS fill of the next stage from `raw`
-// into `nxt`, then the loads of the stage after that into `raw`.
+// s_waitcnt with only the vector-memory count limited (expcnt and lgkmcnt
+// at their maxima).
+template <int N>
+__device__ __forceinline__ void wait_vmcnt() {
+  static_assert(N >= 0 && N < 64, "vmcnt is 6 bits");
+  __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
+}
+
+// A full stage: MFMAs on `cur`, the next stage's dY (DMA) and X (from `raw`)
+// into `nxt`, then the loads of the stage after that into `raw`.  Before the
+// barrier every thread waits for its own DMA (the X loads issued after it
+// may stay in flight); the barrier then publishes the whole tile.
 template <int CODE, int BLOCK>
-__device__ __forceinline__ void stage(f32x16 (&acc)[4][2], const uint8_t *cur, uint8_t *nxt,
-                                      Stage &raw, const WgradArgs &a, int64_t k_load,
-                                      const LoadPlan &lp, int wm, int wn, int lrow, int lk,
-                                      int lc, int g) {
-  const StageRsrc rs = stage_rsrc<BLOCK>(a, k_load);
+__device__ __forceinline__ void stage(f32x16 (&acc)[4][2], const uint8_t *cur_a,
+                                      const uint8_t *cur_b, uint8_t *nxt_a, uint8_t *nxt_b,
+                                      Stage &raw, const WgradArgs &a, int64_t k_next,
+                                      const LoadPlan &lp, const FragPlan &fp, int wave, int lc,
+                                      int g) {
+  const __amdgpu_buffer_rsrc_t ry = y_rsrc(a, k_next);
+  const XRsrc rx = x_rsrc<BLOCK>(a, k_next + BK);
   Frags f;
-  read_frags<0>(f, cur, wm, wn, lrow, lk);
-  region<CODE, 0>(acc, f, cur, nxt, raw, rs, lp, wm, wn, lrow, lk, lc, g);
-  region<CODE, 1>(acc, f, cur, nxt, raw, rs, lp, wm, wn, lrow, lk, lc, g);
-  region<CODE, 2>(acc, f, cur, nxt, raw, rs, lp, wm, wn, lrow, lk, lc, g);
-  region<CODE, 3>(acc, f, cur, nxt, raw, rs, lp, wm, wn, lrow, lk, lc, g);
+  read_frags<0>(f, cur_a, cur_b, fp);
+  region<CODE, 0>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
+  region<CODE, 1>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
+  region<CODE, 2>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
+  region<CODE, 3>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
+  wait_vmcnt<kXLoads>();
   __syncthreads();
-}
-
-template <int CODE>
-__device__ __forceinline__ void fill_stage(const Stage &st, uint8_t *lds_a, int lc, int g) {
-  fill_quarter<CODE, 0>(st, lds_a, lc, g);
-  fill_quarter<CODE, 1>(st, lds_a, lc, g);
-  fill_quarter<CODE, 2>(st, lds_a, lc, g);
-  fill_quarter<CODE, 3>(st, lds_a, lc, g);
 }
 
 template <int CODE, int BLOCK>
 __global__ __launch_bounds__(kThreads, 1) void wgrad_kernel(const WgradArgs a, int tiles_m,
                                                             int tiles_n) {
-  // Stage buffer b holds A at lds + 2b * kTileBytes and B right after it.
-  __shared__ __attribute__((aligned(16))) uint8_t lds[4 * kTileBytes];
+  // Two stage buffers, each an A (dequantised X) and a B (dY) tile; separate
+  // arrays so that the compiler can tell the DMA targets from the tiles
+  // being read.
+  __shared__ __attribute__((aligned(16))) uint8_t lds_a0[kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_b0[kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_a1[kTileBytes];
+  __shared__ __attribute__((aligned(16))) uint8_t lds_b1[kTileBytes];
 
   // XCD-aware tile order.
   const int n_wg = tiles_m * tiles_n;
@@ -280,22 +318,44 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_kernel(const WgradArgs a, i
   const int64_t m0 = (int64_t)tm * BM, n0 = (int64_t)tn * BN;
 
   const int tid = threadIdx.x;
-  const int wave = tid >> 6;
+  const int wave = __builtin_amdgcn_readfirstlane(tid >> 6);
   const int lane = tid & 63;
-  const int wm = wave >> 2, wn = wave & 3;
-  const int lrow = lane & 31, lk = lane >> 5;
-  const int lc = tid & 63, g = tid >> 6;  // loader: 4-column chunk lc, token rows 8 g .. 8 g + 7
+  const int wn = wave & 3;
+  const int lc = tid & 63, g = tid >> 6;  // X loader: 4-column chunk lc, token rows 8 g .. 8 g + 7
 
   LoadPlan lp;
   {
     const uint32_t kg = (uint32_t)g * 8u;
-    const int64_t m = m0 + lc * 4, n = n0 + lc * 4;
+    const int64_t m = m0 + lc * 4;
     lp.st_x = (uint32_t)a.M;
     lp.st_s = (uint32_t)(a.M / BLOCK) * 4u;
-    lp.st_y = (uint32_t)a.N * 2u;
     lp.vo_x = m < a.M ? kg * lp.st_x + (uint32_t)m : kOob;
     lp.vo_s = m < a.M ? kg * lp.st_s + (uint32_t)(m / BLOCK) * 4u : kOob;
-    lp.vo_y = n < a.N ? kg * lp.st_y + (uint32_t)n * 2u : kOob;
+#pragma unroll
+    for (int r = 0; r < 4; ++r) {
+      const uint32_t t = (uint32_t)(wave * 8 + 2 * r + (lane >> 5));
+      const uint32_t c = (uint32_t)(lane & 31) ^ y_swz(t);
+      const int64_t n = n0 + 8 * c;
+      lp.vo_y[r] = n < a.N ? t * (uint32_t)a.N * 2u + (uint32_t)n * 2u : kOob;
+    }
+  }
+  FragPlan fp;
+  {
+    fp.wm = wave >> 2;
+    fp.lrow = lane & 31;
+    fp.lk = lane >> 5;
+    // transposing reads: 16-lane group q = lane / 16, lane 4 a' + c' within
+    // it addresses row e = (lane & 15) / 4 of a 4-row slice, columns 4 a
+    // .. 4 a + 3 (a = lane & 3) of the group's 16-column half
+    const uint32_t q = (uint32_t)lane >> 4, e = ((uint32_t)lane & 15u) >> 2, a4 = lane & 3;
+    const uint32_t t = 8u * (q >> 1) + e;                          // t at k-step 0, read 0
+    const uint32_t col = 16u * (q & 1u) + 4u * a4;                 // within the 32-column block
+    const uint32_t swz = (e << 2) | ((q >> 1) << 4);               // y_swz(t) at every k-step
+#pragma unroll
+    for (int j = 0; j < 2; ++j) {
+      const uint32_t chunk = (uint32_t)(wn * 64 + j * 32 + col) >> 3;
+      fp.yb[j] = t * 512u + ((chunk ^ swz) << 4) + (col & 7u) * 2u;
+    }
   }
 
   f32x16 acc[4][2];
@@ -304,22 +364,26 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_kernel(const WgradArgs a, i
 #pragma unroll
     for (int j = 0; j < 2; ++j) acc[i][j] = f32x16{};
 
-  // Stage s lives in LDS buffer s % 2; the raw operands of stage s+1 wait in
-  // registers.  Loads of stages past K read nothing (empty buffer range) and
-  // return 0, so the loop needs no edge branches; the stage count is rounded
-  // up to even so that the buffer of every stage is a compile-time constant.
+  // Stage s lives in LDS buffer s % 2; the raw X operand of stage s+1 waits
+  // in registers.  Loads of stages past K read nothing (empty buffer range)
+  // and return 0, so the loop needs no edge branches; the stage count is
+  // rounded up to even so that the buffer of every stage is a compile-time
+  // constant.
   const int64_t n_stages = ((a.K + BK - 1) / BK + 1) & ~int64_t(1);
   Stage raw;
-  load_stage(raw, stage_rsrc<BLOCK>(a, 0), lp);
-  fill_stage<CODE>(raw, lds, lc, g);
-  load_stage(raw, stage_rsrc<BLOCK>(a, BK), lp);
+  dma_dy(y_rsrc(a, 0), lp, lds_b0, wave);
+  load_stage(raw, x_rsrc<BLOCK>(a, 0), lp);
+  fill_x<CODE, 0>(raw, lds_a0, lc, g);
+  fill_x<CODE, 2>(raw, lds_a0, lc, g);
+  load_stage(raw, x_rsrc<BLOCK>(a, BK), lp);
+  wait_vmcnt<kXLoads>();
   __syncthreads();
 
-  uint8_t *const buf0 = lds;
-  uint8_t *const buf1 = lds + 2 * kTileBytes;
   for (int64_t s = 0; s < n_stages; s += 2) {
-    stage<CODE, BLOCK>(acc, buf0, buf1, raw, a, (s + 2) * BK, lp, wm, wn, lrow, lk, lc, g);
-    stage<CODE, BLOCK>(acc, buf1, buf0, raw, a, (s + 3) * BK, lp, wm, wn, lrow, lk, lc, g);
+    stage<CODE, BLOCK>(acc, lds_a0, lds_b0, lds_a1, lds_b1, raw, a, (s + 1) * BK, lp, fp, wave,
+                       lc, g);
+    stage<CODE, BLOCK>(acc, lds_a1, lds_b1, lds_a0, lds_b0, raw, a, (s + 2) * BK, lp, fp, wave,
+                       lc, g);
   }
 
   // Epilogue.  32x32 accumulator layout: lane l holds column l % 32 and, for
@@ -328,10 +392,10 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_kernel(const WgradArgs a, i
   for (int i = 0; i < 4; ++i) {
 #pragma unroll
     for (int j = 0; j < 2; ++j) {
-      const int64_t col = n0 + wn * 64 + j * 32 + lrow;
+      const int64_t col = n0 + wn * 64 + j * 32 + fp.lrow;
 #pragma unroll
       for (int r = 0; r < 16; ++r) {
-        const int64_t row = m0 + wm * 128 + i * 32 + (r >> 2) * 8 + lk * 4 + (r & 3);
+        const int64_t row = m0 + fp.wm * 128 + i * 32 + (r >> 2) * 8 + fp.lk * 4 + (r & 3);
         if (row < a.M && col < a.N) {
           float *p = a.dw + row * a.N + col;
           *p = a.accumulate ? *p + acc[i][j][r] : acc[i][j][r];
