@@ -43,6 +43,8 @@ def parse():
     p.add_argument("--no-cpu-baseline", action="store_true")
     p.add_argument("--copy-calibration", action="store_true",
                    help="also run a plain 1 GiB device copy (for scaling HBM byte counters)")
+    p.add_argument("--blas-ref", action="store_true",
+                   help="also time hipBLASLt's bf16 GEMM (torch.mm) on the reconstructed X, for context")
     p.add_argument("--cpu-rows", type=int, default=8192,
                    help="MLP rows (and 4x as many hidden rows) in the oracle's timed sample")
     return p.parse_args()
@@ -263,11 +265,41 @@ def main():
         "rooflines": roofs,
     }
 
+    if args.blas_ref:
+        progress("timing hipBLASLt on the reconstructed X")
+        out["blas_ref"] = blas_ref(sets[0], code, block, K, M, N)
     if not args.no_cpu_baseline:
         progress("timing the oracle on the host")
         out["cpu_baseline"] = cpu_baseline(args, sets[0], w, block, code)
     print(json.dumps(out))
     return 0
+
+
+def blas_ref(st, code, block, K, M, N, iters=10):
+    """Context only: the library GEMM (torch.mm -> hipBLASLt, bf16 in, bf16
+    out, fp32 accumulation) on X reconstructed by hilore_decompress, with X^T
+    as a transposed view (the layout the fused kernel reads) and after making
+    it contiguous.  Not part of the hot path."""
+    import torch
+    from paper_2609_33570_amd import hilore as hl
+
+    xhat = torch.empty((K, M), dtype=torch.bfloat16, device="cuda")
+    hl.hilore_decompress([hl.unit_desc(codes=st["wc"], scales=st["ws"], xhat=xhat)], code, block)
+    xt = xhat.t().contiguous()
+    res = {}
+    for name, a in (("xhatT_view", xhat.t()), ("xhatT_contiguous", xt)):
+        for _ in range(3):
+            torch.mm(a, st["dy"])
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        for _ in range(iters):
+            torch.mm(a, st["dy"])
+        e1.record()
+        torch.cuda.synchronize()
+        ms = e0.elapsed_time(e1) / iters
+        res[f"tflops_{name}"] = round(2.0 * K * M * N / (ms * 1e-3) / 1e12, 2)
+    res["what"] = "torch.mm bf16 on the reconstructed X (hipBLASLt), same K, M, N; context, not a target"
+    return res
 
 
 def cpu_baseline(args, st, w, block, code):

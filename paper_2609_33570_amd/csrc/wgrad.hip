@@ -34,8 +34,8 @@
 // starts the DMA of stage s+1's dY into the other buffer; regions 2 and 3
 // dequantise stage s+1's X (already in registers) into that buffer, and
 // region 3 then issues the global loads of stage s+2's X into the same
-// registers.  Every region reads the next k-step's fragments after its
-// MFMAs.  A wait for this thread's DMA and one barrier end the stage.
+// registers.  Every region reads the next k-step's fragments while its
+// MFMAs issue.  A wait for this thread's DMA and one barrier end the stage.
 //
 // Work distribution: workgroups are dealt round-robin to the 8 XCDs; the
 // launch index is remapped so that each XCD receives a contiguous run of
@@ -219,10 +219,33 @@ __device__ __forceinline__ void mma8(f32x16 (&acc)[4][2], const Frags &f) {
       acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
 }
 
+// The 8 MFMAs of this k-step with the fragment reads of k-step KS woven in:
+// each A fragment is re-read as soon as its two MFMAs have been issued, the
+// B fragments after the last one, so the reads start up to six MFMAs
+// earlier than after the whole block.
+template <int KS>
+__device__ __forceinline__ void mma8_read(f32x16 (&acc)[4][2], Frags &f, const uint8_t *al,
+                                          const uint8_t *bl, const FragPlan &fp) {
+#pragma unroll
+  for (int i = 0; i < 4; ++i) {
+    acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[0], acc[i][0], 0, 0, 0);
+    acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[1], acc[i][1], 0, 0, 0);
+    f.a[i] = *reinterpret_cast<const bf16x8 *>(
+        al + lds_off(fp.wm * 128 + i * 32 + fp.lrow, KS * 2 + fp.lk));
+  }
+#pragma unroll
+  for (int j = 0; j < 2; ++j) {
+    const s16x4 lo = read_tr16(bl + fp.yb[j] + KS * 16 * 512);
+    const s16x4 hi = read_tr16(bl + fp.yb[j] + (KS * 16 + 4) * 512);
+    f.b[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+  }
+}
+
 // Instruction order of one k-step region: every MFMA followed by VALU ops
 // of the next stage's dequantisation (last two regions), LDS stores spread
-// over the region, global loads after the first MFMAs, then the LDS reads of
-// the next k-step's fragments.
+// over the region, global loads after the first MFMAs, and the LDS reads of
+// the next k-step's fragments: one A fragment after every second MFMA, the
+// rest after the last.
 template <bool NEXT, int VALU, int WRITES, int LOADS>
 __device__ __forceinline__ void schedule_region() {
 #pragma unroll
@@ -233,8 +256,10 @@ __device__ __forceinline__ void schedule_region() {
       if (i % (8 / WRITES) == 8 / WRITES - 1) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
     if constexpr (LOADS > 0)
       if (i < (LOADS + 1) / 2) __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
+    if constexpr (NEXT)
+      if (i == 1 || i == 3 || i == 5) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
-  if constexpr (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, 8, 0);  // 8 LDS reads
+  if constexpr (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, 5, 0);  // 5 more LDS reads
   __builtin_amdgcn_sched_barrier(0);
 }
 
@@ -244,7 +269,8 @@ __device__ __forceinline__ void schedule_region() {
 // that into the same registers (so one register set suffices and the loads
 // have until region 2 of the next stage to land).  The fragments of the next
 // k-step are read into the same registers once this k-step's MFMAs have been
-// issued; the other wave on the SIMD covers that latency.
+// issued (each A fragment as soon as its MFMAs are); the other wave on the
+// SIMD covers the rest of that latency.
 template <int CODE, int KS>
 __device__ __forceinline__ void region(f32x16 (&acc)[4][2], Frags &f, const uint8_t *cur_a,
                                        const uint8_t *cur_b, uint8_t *nxt_a, uint8_t *nxt_b,
@@ -257,8 +283,8 @@ __device__ __forceinline__ void region(f32x16 (&acc)[4][2], Frags &f, const uint
     fill_x<CODE, 2>(raw, nxt_a, lc, g);
     load_stage(raw, rx, lp);
   }
-  mma8(acc, f);
-  if constexpr (KS < 3) read_frags<KS + 1>(f, cur_a, cur_b, fp);
+  if constexpr (KS < 3) mma8_read<KS + 1>(acc, f, cur_a, cur_b, fp);
+  if constexpr (KS == 3) mma8(acc, f);
   if constexpr (KS == 0) schedule_region<true, 0, 0, kYLoads>();
   if constexpr (KS == 1) schedule_region<true, 0, 0, 0>();
   if constexpr (KS == 2) schedule_region<true, 4, 2, 0>();
