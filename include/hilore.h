@@ -49,14 +49,23 @@ typedef enum hilore_status {
 } hilore_status;
 
 typedef enum hilore_code {
-  HILORE_CODE_INT8 = 0,       /* two's-complement int8, symmetric range [-127, 127] */
-  HILORE_CODE_FP8_E4M3FN = 1  /* OCP E4M3FN (torch.float8_e4m3fn), max 448          */
+  HILORE_CODE_INT8 = 0,            /* two's-complement int8, symmetric range [-127, 127],
+                                      one fp32 scale per block                          */
+  HILORE_CODE_FP8_E4M3FN = 1,      /* OCP E4M3FN (torch.float8_e4m3fn), max 448,
+                                      one fp32 scale per block                          */
+  HILORE_CODE_FP8_E4M3FN_CAST = 2  /* the paper's literal codec (App. B.1 Eq.
+                                      fp8-roundtrip): a plain E4M3FN cast of each bf16
+                                      value, no scales (block must be 0, scales unused).
+                                      Identical to torch.float8_e4m3fn: nearest-even,
+                                      NOT saturating: |x| > 464, +-inf and NaN give the
+                                      NaN code 0x7F | sign; (448, 464] gives +-448.  The
+                                      cast back is exact; a NaN code gives bf16 0x7FC0. */
 } hilore_code;
 
 /* One recovery unit: one saved bf16 activation tensor that receives a single
  * H/L/R action across all its tokens (Sec. 3.4).  Rows are tokens of the
  * microbatch, columns are features; blocks of `block` consecutive columns of
- * one row share one fp32 scale.
+ * one row share one fp32 scale (no scales with HILORE_CODE_FP8_E4M3FN_CAST).
  *   x          bf16 [rows, cols], row stride ld elements (ld >= cols, ld % 8 == 0)
  *   codes      [rows, cols] dense, one byte per element
  *   scales     fp32 [rows, cols / block] dense
@@ -133,15 +142,21 @@ hilore_status hilore_grpo_coeffs(const float *rewards, const float *logp_new,
  * error of Eq. app-calibration-error), accumulated in a fixed order.
  *   units[n_units]  host array; uses x, codes, scales, row_ss_x, row_ss_err, rows, cols, ld
  *   block           32, 64, 128 or 256; every unit needs cols % block == 0
+ * With code HILORE_CODE_FP8_E4M3FN_CAST (block = 0) each element is cast on its
+ * own, scales are neither read nor written, and xhat in the row sums is the
+ * cast back (a NaN code makes its row's ss_err NaN).
  * All units of one call are encoded on `stream`; they may differ in shape.
+ * Errors: bad code, or block != 0 with the cast code -> INVALID_ARG; other
+ * block sizes -> UNSUPPORTED.
  */
 hilore_status hilore_compress(const hilore_unit_desc *units, int n_units, int code, int block,
                               void *stream);
 
 /*
  * Reconstruction of L units for backward (App. B.1 Eq. fp8-roundtrip, the cast
- * back to bf16): xhat = bf16_RNE(value(code) * scale), elementwise.
- *   units[n_units]  host array; uses codes, scales, xhat, rows, cols
+ * back to bf16): xhat = bf16_RNE(value(code) * scale), elementwise; with
+ * HILORE_CODE_FP8_E4M3FN_CAST xhat = value(code) exactly (NaN codes -> 0x7FC0).
+ *   units[n_units]  host array; uses codes, scales (not with the cast code), xhat, rows, cols
  */
 hilore_status hilore_decompress(const hilore_unit_desc *units, int n_units, int code,
                                 int block, void *stream);
@@ -177,6 +192,8 @@ hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask,
  *   dy       bf16 [K, N]; dw f32 [M, N] row-major (the transpose of a [N, M] weight's layout)
  *   accumulate: 0 overwrites dw, 1 adds to it
  * bf16 x bf16 products, fp32 accumulation (MFMA).  xhat is never written to memory.
+ * With HILORE_CODE_FP8_E4M3FN_CAST (block = 0, x_scales unused, may be NULL)
+ * xhat = value(code) exactly; a NaN code makes its row of dW NaN.
  * Limits: M % block == 0, M % 8 == 0, N % 8 == 0, K >= 0 (K = 0 writes zeros or leaves dw).
  */
 hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, int code,

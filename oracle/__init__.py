@@ -22,6 +22,7 @@ _LIB = os.path.join(_HERE, "liboracle.so")
 
 INT8 = 0
 E4M3FN = 1
+E4M3FN_CAST = 2  # the paper's literal codec: a plain cast, no scales
 
 GCC_FLAGS = ["-O2", "-std=c11", "-Wall", "-Wextra", "-ffp-contract=off", "-fno-fast-math",
              "-fPIC", "-shared"]
@@ -55,6 +56,9 @@ def lib() -> ctypes.CDLL:
             "orc_bf16_rne": (ctypes.c_uint16, [f32]),
             "orc_e4m3fn_rne": (ctypes.c_uint8, [f32]),
             "orc_e4m3fn_decode": (f64, [ctypes.c_uint8]),
+            "orc_e4m3fn_cast": (ctypes.c_uint8, [f32]),
+            "orc_e4m3fn_cast_to_bf16": (ctypes.c_uint16, [ctypes.c_uint8]),
+            "orc_e4m3fn_cast_array": (None, [P, i64, P]),
             "orc_code_value": (f32, [i32, ctypes.c_uint8]),
             "orc_bf16_rne_array": (None, [P, i64, P]),
             "orc_e4m3fn_rne_array": (None, [P, i64, P]),
@@ -107,6 +111,17 @@ def e4m3fn_rne(v):
     return out
 
 
+def e4m3fn_cast(v):
+    v = _c(v, np.float32).ravel()
+    out = np.empty(v.size, dtype=np.uint8)
+    lib().orc_e4m3fn_cast_array(_ptr(v), v.size, _ptr(out))
+    return out
+
+
+def e4m3fn_cast_to_bf16(c: int) -> int:
+    return lib().orc_e4m3fn_cast_to_bf16(int(c))
+
+
 def e4m3fn_decode(c: int) -> float:
     return lib().orc_e4m3fn_decode(int(c))
 
@@ -155,12 +170,13 @@ def grpo_loss(adv, logp_new_f64, logp_old, logp_ref, mask, R, T, clip_eps=0.2, b
 # ------------------------------------------------------------------ codec --
 def quantize(x_u16, code, block, cols=None):
     """x_u16: uint16 [rows, ld] bf16 bits (ld = row stride); quantises the first
-    ``cols`` columns of every row (all of them by default)."""
+    ``cols`` columns of every row (all of them by default).  With the literal
+    cast code the scales are None."""
     x = _c(x_u16, np.uint16)
     rows, ld = x.shape
     cols = ld if cols is None else cols
     codes = np.empty((rows, cols), dtype=np.uint8)
-    scales = np.empty((rows, cols // block), dtype=np.float32)
+    scales = None if code == E4M3FN_CAST else np.empty((rows, cols // block), dtype=np.float32)
     lib().orc_quantize(_ptr(x), rows, cols, ld, code, block, _ptr(codes), _ptr(scales))
     return codes, scales
 

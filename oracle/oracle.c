@@ -56,15 +56,12 @@ double orc_e4m3fn_decode(uint8_t c) {
   return s ? -mag : mag;
 }
 
-/* fp32 -> E4M3FN, round to nearest with ties to even on the E4M3FN grid,
- * saturating at +-448, keeping the sign of zero.  Done by exact arithmetic in
- * double: the grid spacing in the binade of |v| is 2^(max(e,-6)-3); round
- * |v| / spacing to the nearest integer (ties to the even integer), multiply
- * back, then encode the resulting grid value. */
-uint8_t orc_e4m3fn_rne(float v) {
-  uint8_t sign = (bits_from_f32(v) >> 31) ? 0x80 : 0x00;
-  double a = fabs((double)v);
-  if (a == 0.0) return sign;
+/* |v| rounded to nearest, ties to even, on the E4M3FN grid continued past
+ * its top (448, 480, 512, ...): exact arithmetic in double.  The grid spacing
+ * in the binade of |v| is 2^(max(e,-6)-3); round |v| / spacing to the nearest
+ * integer (ties to the even integer) and multiply back. */
+static double e4m3fn_round_mag(double a) {
+  if (a == 0.0) return 0.0;
   int ex;
   frexp(a, &ex);                                /* a = f * 2^ex, f in [0.5,1) */
   int e = ex - 1;                               /* a in [2^e, 2^(e+1)) */
@@ -75,19 +72,46 @@ uint8_t orc_e4m3fn_rne(float v) {
   if (frac > 0.5) k = fl + 1.0;
   else if (frac < 0.5) k = fl;
   else k = (fmod(fl, 2.0) == 0.0) ? fl : fl + 1.0;
-  double g = ldexp(k, qe);                      /* rounded grid value */
+  return ldexp(k, qe);
+}
+
+/* Code bits of a grid value g in [0, 448]. */
+static uint8_t e4m3fn_encode_mag(double g) {
+  if (g < ldexp(1.0, -6)) return (uint8_t)ldexp(g, 9); /* subnormal: g = m * 2^-9 */
+  int gx;
+  frexp(g, &gx);
+  int ge = gx - 1;                              /* g in [2^ge, 2^(ge+1)) */
+  int mant = (int)ldexp(g, 3 - ge) - 8;         /* 3-bit mantissa */
+  return (uint8_t)(((ge + 7) << 3) | mant);
+}
+
+/* fp32 -> E4M3FN, round to nearest with ties to even on the E4M3FN grid,
+ * saturating at +-448, keeping the sign of zero. */
+uint8_t orc_e4m3fn_rne(float v) {
+  uint8_t sign = (bits_from_f32(v) >> 31) ? 0x80 : 0x00;
+  double g = e4m3fn_round_mag(fabs((double)v));
   if (g > 448.0) g = 448.0;                     /* saturate */
-  uint8_t code;
-  if (g < ldexp(1.0, -6)) {
-    code = (uint8_t)ldexp(g, 9);                /* subnormal: g = m * 2^-9, m in 0..7 */
-  } else {
-    int gx;
-    frexp(g, &gx);
-    int ge = gx - 1;                            /* g in [2^ge, 2^(ge+1)) */
-    int mant = (int)ldexp(g, 3 - ge) - 8;       /* 3-bit mantissa */
-    code = (uint8_t)(((ge + 7) << 3) | mant);
-  }
-  return (uint8_t)(sign | code);
+  return (uint8_t)(sign | e4m3fn_encode_mag(g));
+}
+
+/* The paper's literal codec (App. B.1, Eq. fp8-roundtrip: a torch.float8_e4m3fn
+ * cast, no scale): the same rounding without saturation.  A value whose
+ * rounded magnitude passes 448 (|v| > 464), an infinity or a NaN has no
+ * E4M3FN encoding and becomes NaN, S.1111.111, keeping the sign. */
+uint8_t orc_e4m3fn_cast(float v) {
+  uint8_t sign = (bits_from_f32(v) >> 31) ? 0x80 : 0x00;
+  if (isnan(v) || isinf(v)) return (uint8_t)(sign | 0x7F);
+  double g = e4m3fn_round_mag(fabs((double)v));
+  if (g > 448.0) return (uint8_t)(sign | 0x7F);
+  return (uint8_t)(sign | e4m3fn_encode_mag(g));
+}
+
+/* The cast back to bf16 of Eq. fp8-roundtrip: every finite E4M3FN value is a
+ * bf16 value, so the conversion is exact; a NaN code becomes the canonical
+ * bf16 NaN 0x7FC0, whatever its sign (torch's float8 -> bfloat16 conversion). */
+uint16_t orc_e4m3fn_cast_to_bf16(uint8_t c) {
+  if ((c & 0x7F) == 0x7F) return 0x7FC0;
+  return orc_bf16_rne((float)orc_e4m3fn_decode(c));
 }
 
 void orc_bf16_rne_array(const float *v, int64_t n, uint16_t *out) {
@@ -98,8 +122,12 @@ void orc_e4m3fn_rne_array(const float *v, int64_t n, uint8_t *out) {
   for (int64_t i = 0; i < n; ++i) out[i] = orc_e4m3fn_rne(v[i]);
 }
 
+void orc_e4m3fn_cast_array(const float *v, int64_t n, uint8_t *out) {
+  for (int64_t i = 0; i < n; ++i) out[i] = orc_e4m3fn_cast(v[i]);
+}
+
 float orc_code_value(int code, uint8_t c) {
-  if (code == ORC_INT8) return (float)(int8_t)c;
+  if (code == ORC_INT8) return (float)(int8_t)c;   /* E4M3FN and the literal cast decode alike */
   return (float)orc_e4m3fn_decode(c);
 }
 
@@ -239,6 +267,12 @@ double orc_grpo_loss(const float *adv, const double *logp_new, const float *logp
  *         E4M3FN: q_j = orc_e4m3fn_rne(v_j). */
 void orc_quantize(const uint16_t *x, int64_t rows, int64_t cols, int64_t ld, int code,
                   int block, uint8_t *codes, float *scales) {
+  if (code == ORC_E4M3FN_CAST) {                /* literal codec: no blocks, no scales */
+    for (int64_t row = 0; row < rows; ++row)
+      for (int64_t c = 0; c < cols; ++c)
+        codes[row * cols + c] = orc_e4m3fn_cast(orc_bf16_to_f32(x[row * ld + c]));
+    return;
+  }
   const float Q = (code == ORC_INT8) ? 127.0f : 448.0f;
   const float tiny = ldexpf(1.0f, -64);
   const int64_t nb = cols / block;
@@ -278,6 +312,10 @@ void orc_quantize(const uint16_t *x, int64_t rows, int64_t cols, int64_t ld, int
  * xhat = bf16_rne( value(q) * s ), the product an fp32 multiply. */
 void orc_dequantize(const uint8_t *codes, const float *scales, int64_t rows, int64_t cols,
                     int code, int block, uint16_t *xhat) {
+  if (code == ORC_E4M3FN_CAST) {                /* literal codec: cast back, no scale */
+    for (int64_t i = 0; i < rows * cols; ++i) xhat[i] = orc_e4m3fn_cast_to_bf16(codes[i]);
+    return;
+  }
   const int64_t nb = cols / block;
   for (int64_t row = 0; row < rows; ++row)
     for (int64_t c = 0; c < cols; ++c) {
@@ -354,6 +392,8 @@ void orc_unit_exposure_risk(const double *coeff, const uint8_t *mask, int64_t ro
 static double deq_value(const uint8_t *codes, const float *scales, int code, int block,
                         int64_t M, int64_t t, int64_t i, int variant) {
   const uint8_t c = codes[t * M + i];
+  if (code == ORC_E4M3FN_CAST)                  /* exact in bf16: both variants agree */
+    return (double)orc_bf16_to_f32(orc_e4m3fn_cast_to_bf16(c));
   const float s = scales[t * (M / block) + i / block];
   if (variant == 0) {
     const double q = (code == ORC_INT8) ? (double)(int8_t)c : orc_e4m3fn_decode(c);

@@ -30,17 +30,22 @@
 extern "C" {
 #endif
 
-enum { ORC_INT8 = 0, ORC_E4M3FN = 1 };
+/* ORC_E4M3FN_CAST is the paper's literal codec: a plain cast, no scales. */
+enum { ORC_INT8 = 0, ORC_E4M3FN = 1, ORC_E4M3FN_CAST = 2 };
 
 /* ---- number formats --------------------------------------------------- */
 float    orc_bf16_to_f32(uint16_t h);
 uint16_t orc_bf16_rne(float v);            /* fp32 -> bf16, nearest-even, by distances */
 uint8_t  orc_e4m3fn_rne(float v);          /* fp32 -> OCP E4M3FN, nearest-even, saturating */
+uint8_t  orc_e4m3fn_cast(float v);         /* fp32 -> E4M3FN as torch.float8_e4m3fn: nearest-even,
+                                              non-saturating (|v| > 464, inf, NaN -> NaN, sign kept) */
+uint16_t orc_e4m3fn_cast_to_bf16(uint8_t c); /* exact; NaN codes -> 0x7FC0 */
 double   orc_e4m3fn_decode(uint8_t c);     /* exact value of an E4M3FN code (NaN for 0x7f/0xff) */
 float    orc_code_value(int code, uint8_t c); /* exact fp32 value of an int8 / E4M3FN code */
 /* element-wise array forms of the two roundings, for exhaustive checks */
 void     orc_bf16_rne_array(const float *v, int64_t n, uint16_t *out);
 void     orc_e4m3fn_rne_array(const float *v, int64_t n, uint8_t *out);
+void     orc_e4m3fn_cast_array(const float *v, int64_t n, uint8_t *out);
 
 /* ---- GRPO (Sec. 3.1 Eq. grpo-objective; Sec. 3.2 Eq. update-coefficient) */
 void orc_grpo_advantages(const float *rewards, int P, int G, float adv_eps, float *adv);
@@ -54,7 +59,8 @@ double orc_grpo_loss(const float *adv, const double *logp_new, const float *logp
                      const float *logp_ref, const uint8_t *mask, int R, int T,
                      double clip_eps, double beta, double n_norm);
 
-/* ---- blockwise absmax codec (App. B.1 Eq. fp8-roundtrip, scaled reading) */
+/* ---- blockwise absmax codec (App. B.1 Eq. fp8-roundtrip, scaled reading);
+ *      with code ORC_E4M3FN_CAST the literal cast (block and scales unused) */
 void orc_quantize(const uint16_t *x, int64_t rows, int64_t cols, int64_t ld, int code,
                   int block, uint8_t *codes, float *scales);
 void orc_dequantize(const uint8_t *codes, const float *scales, int64_t rows, int64_t cols,

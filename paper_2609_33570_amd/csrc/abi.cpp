@@ -19,7 +19,18 @@ bool aligned16(const void *p) { return (reinterpret_cast<uintptr_t>(p) & 15u) ==
 
 bool valid_block(int block) { return block == 32 || block == 64 || block == 128 || block == 256; }
 
-bool valid_code(int code) { return code == HILORE_CODE_INT8 || code == HILORE_CODE_FP8_E4M3FN; }
+bool valid_code(int code) {
+  return code == HILORE_CODE_INT8 || code == HILORE_CODE_FP8_E4M3FN ||
+         code == HILORE_CODE_FP8_E4M3FN_CAST;
+}
+
+// The blockwise codes need a supported block size; the literal cast has no
+// blocks and takes block == 0.
+hilore_status check_code_block(int code, int block) {
+  if (!valid_code(code)) return HILORE_ERR_INVALID_ARG;
+  if (code == HILORE_CODE_FP8_E4M3FN_CAST) return block == 0 ? HILORE_OK : HILORE_ERR_INVALID_ARG;
+  return valid_block(block) ? HILORE_OK : HILORE_ERR_UNSUPPORTED;
+}
 
 hilore_status hip_status(hipError_t e) { return e == hipSuccess ? HILORE_OK : HILORE_ERR_HIP; }
 
@@ -64,8 +75,9 @@ hilore_status run_codec(const hilore_unit_desc *units, int n_units, int code, in
   if (n_units < 0) return HILORE_ERR_INVALID_ARG;
   if (n_units == 0) return HILORE_OK;
   if (!units) return HILORE_ERR_INVALID_ARG;
-  if (!valid_code(code)) return HILORE_ERR_INVALID_ARG;
-  if (!valid_block(block)) return HILORE_ERR_UNSUPPORTED;
+  const hilore_status cb = check_code_block(code, block);
+  if (cb != HILORE_OK) return cb;
+  if (code == HILORE_CODE_FP8_E4M3FN_CAST) use &= ~unsigned(kUseScales);
   for (int i = 0; i < n_units; ++i) {
     const hilore_status st = check_unit(units[i], block, use);
     if (st != HILORE_OK) return st;
@@ -226,19 +238,20 @@ hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, i
                                    int block, const uint16_t *dy, float *dw, int64_t K,
                                    int64_t M, int64_t N, int accumulate, void *stream) {
   if (K < 0 || M < 0 || N < 0) return HILORE_ERR_INVALID_ARG;
-  if (!valid_code(code)) return HILORE_ERR_INVALID_ARG;
-  if (!valid_block(block)) return HILORE_ERR_UNSUPPORTED;
-  if (M % block != 0 || M % 8 != 0 || N % 8 != 0) return HILORE_ERR_UNSUPPORTED;
+  const hilore_status cb = check_code_block(code, block);
+  if (cb != HILORE_OK) return cb;
+  const bool cast = code == HILORE_CODE_FP8_E4M3FN_CAST;
+  if ((!cast && M % block != 0) || M % 8 != 0 || N % 8 != 0) return HILORE_ERR_UNSUPPORTED;
   if (M / 256 + 1 > (1 << 14) || N / 256 + 1 > (1 << 14)) return HILORE_ERR_UNSUPPORTED;
   if (M == 0 || N == 0) return HILORE_OK;
   if (!dw) return HILORE_ERR_INVALID_ARG;
-  if (K > 0 && (!x_codes || !x_scales || !dy)) return HILORE_ERR_INVALID_ARG;
+  if (K > 0 && (!x_codes || (!cast && !x_scales) || !dy)) return HILORE_ERR_INVALID_ARG;
   const void *ptrs[] = {x_codes, x_scales, dy, dw};
   for (const void *p : ptrs)
     if (p && !aligned16(p)) return HILORE_ERR_ALIGNMENT;
   hilore::WgradArgs a{};
   a.codes = static_cast<const uint8_t *>(x_codes);
-  a.scales = x_scales;
+  a.scales = cast ? nullptr : x_scales;
   a.dy = dy;
   a.dw = dw;
   a.K = K;

@@ -17,6 +17,12 @@
 // order and reduced once per row with a butterfly, so they do not depend on
 // the grid size.
 //
+// The literal codec (code kCodeCast) is the paper's plain cast with no scale:
+// code = E4M3FN nearest-even of x where |x| <= 464 (448 for (448, 464]),
+// NaN (S.1111.111, sign kept) where |x| > 464 or x is not finite, exactly as
+// torch.float8_e4m3fn casts; the cast back is exact, NaN codes giving the
+// canonical bf16 NaN 0x7FC0.
+//
 // Exact quotients without a divide.  amax is the magnitude of one of the
 // block's bf16 elements, so amax = m * 2^e with m one of the 128 bf16
 // mantissas 1 + k/128.  Because scaling by a power of two commutes with
@@ -132,6 +138,130 @@ __device__ __forceinline__ void decode8(u32x2 c, float q[8]) {
     d = __builtin_amdgcn_cvt_pk_f32_fp8((int)c.x, true);  q[2] = d.x; q[3] = d.y;
     d = __builtin_amdgcn_cvt_pk_f32_fp8((int)c.y, false); q[4] = d.x; q[5] = d.y;
     d = __builtin_amdgcn_cvt_pk_f32_fp8((int)c.y, true);  q[6] = d.x; q[7] = d.y;
+  }
+}
+
+// The literal cast of 8 values (see the file comment); q[] receives the
+// exact values of the codes (NaN for NaN codes).
+__device__ __forceinline__ u32x2 cast8(const float x[8], float q[8]) {
+  int lo = __builtin_amdgcn_cvt_pk_fp8_f32(x[0], x[1], 0, false);
+  lo = __builtin_amdgcn_cvt_pk_fp8_f32(x[2], x[3], lo, true);
+  int hi = __builtin_amdgcn_cvt_pk_fp8_f32(x[4], x[5], 0, false);
+  hi = __builtin_amdgcn_cvt_pk_fp8_f32(x[6], x[7], hi, true);
+  uint32_t w[2] = {(uint32_t)lo, (uint32_t)hi};
+#pragma unroll
+  for (int i = 0; i < 8; ++i) {
+    // |x| > 464, infinities and NaNs (all of whose magnitude bits exceed those
+    // of 464.0f) have no encoding: NaN with the sign of x
+    const uint32_t xb = __float_as_uint(x[i]);
+    const uint32_t nan = 0x7Fu | ((xb >> 24) & 0x80u);
+    const int sh = 8 * (i & 3);
+    uint32_t &wd = w[i >> 2];
+    wd = (xb & 0x7FFFFFFFu) > 0x43E80000u ? (wd & ~(0xFFu << sh)) | (nan << sh) : wd;
+  }
+  const u32x2 out = {w[0], w[1]};
+  f32x2 d;
+  d = __builtin_amdgcn_cvt_pk_f32_fp8((int)out.x, false); q[0] = d.x; q[1] = d.y;
+  d = __builtin_amdgcn_cvt_pk_f32_fp8((int)out.x, true);  q[2] = d.x; q[3] = d.y;
+  d = __builtin_amdgcn_cvt_pk_f32_fp8((int)out.y, false); q[4] = d.x; q[5] = d.y;
+  d = __builtin_amdgcn_cvt_pk_f32_fp8((int)out.y, true);  q[6] = d.x; q[7] = d.y;
+  return out;
+}
+
+// bf16 of two E4M3FN codes (bytes 2k, 2k+1 of w, k = HI): exact, NaN codes
+// -> 0x7FC0.
+template <bool HI>
+__device__ __forceinline__ uint32_t uncast2(uint32_t w) {
+  const f32x2 d = __builtin_amdgcn_cvt_pk_f32_fp8((int)w, HI);
+  uint32_t lo = __float_as_uint(d.x) >> 16, hi = __float_as_uint(d.y) >> 16;  // exact
+  const uint32_t c0 = (w >> (HI ? 16 : 0)) & 0x7Fu, c1 = (w >> (HI ? 24 : 8)) & 0x7Fu;
+  lo = c0 == 0x7Fu ? 0x7FC0u : lo;
+  hi = c1 == 0x7Fu ? 0x7FC0u : hi;
+  return lo | (hi << 16);
+}
+
+// The literal cast, same row-per-wave mapping as compress_kernel.
+template <bool STATS>
+__global__ __launch_bounds__(kThreads) void cast_kernel(const CodecBatch b) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t n_waves = (int64_t)gridDim.x * kWavesPerBlock;
+  const int64_t total = b.row_begin[b.n];
+  for (int64_t g = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; g < total;
+       g += n_waves) {
+    const int u = find_unit(b, g);
+    const CodecUnit &d = b.u[u];
+    const int64_t row = g - b.row_begin[u];
+    const int64_t cols = d.cols;
+    const u32x4 *xr = reinterpret_cast<const u32x4 *>(d.x + row * d.ld);
+    u32x2 *cr = reinterpret_cast<u32x2 *>(d.codes + row * cols);
+    float acc_x = 0.0f, acc_e = 0.0f;
+    for (int64_t c0 = 0; c0 < cols; c0 += kColsPerStep * kUnroll) {
+      u32x4 w[kUnroll];
+#pragma unroll
+      for (int i = 0; i < kUnroll; ++i) {
+        const int64_t col = c0 + i * kColsPerStep + lane * 8;
+        w[i] = col < cols ? __builtin_nontemporal_load(xr + col / 8) : u32x4{0, 0, 0, 0};
+      }
+#pragma unroll
+      for (int i = 0; i < kUnroll; ++i) {
+        const int64_t col = c0 + i * kColsPerStep + lane * 8;
+        if (col >= cols) continue;
+        float x[8], q[8];
+        x[0] = bf16_lo(w[i].x); x[1] = bf16_hi(w[i].x);
+        x[2] = bf16_lo(w[i].y); x[3] = bf16_hi(w[i].y);
+        x[4] = bf16_lo(w[i].z); x[5] = bf16_hi(w[i].z);
+        x[6] = bf16_lo(w[i].w); x[7] = bf16_hi(w[i].w);
+        __builtin_nontemporal_store(cast8(x, q), cr + col / 8);
+        if constexpr (STATS) {
+#pragma unroll
+          for (int j = 0; j < 8; ++j) {
+            const float e = q[j] - x[j];  // exact: both are bf16 values (or NaN)
+            acc_e = fmaf(e, e, acc_e);
+            acc_x = fmaf(x[j], x[j], acc_x);
+          }
+        }
+      }
+    }
+    if constexpr (STATS) {
+      acc_x = wave_sum(acc_x);
+      acc_e = wave_sum(acc_e);
+      if (lane == 0) {
+        if (d.ss_x) d.ss_x[row] = acc_x;
+        if (d.ss_err) d.ss_err[row] = acc_e;
+      }
+    }
+  }
+}
+
+__global__ __launch_bounds__(kThreads) void uncast_kernel(const CodecBatch b) {
+  const int lane = threadIdx.x & (kWave - 1);
+  const int64_t n_waves = (int64_t)gridDim.x * kWavesPerBlock;
+  const int64_t total = b.row_begin[b.n];
+  for (int64_t g = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; g < total;
+       g += n_waves) {
+    const int u = find_unit(b, g);
+    const CodecUnit &d = b.u[u];
+    const int64_t row = g - b.row_begin[u];
+    const int64_t cols = d.cols;
+    const u32x2 *cr = reinterpret_cast<const u32x2 *>(d.codes + row * cols);
+    u32x4 *hr = reinterpret_cast<u32x4 *>(d.xhat + row * cols);
+    for (int64_t c0 = 0; c0 < cols; c0 += kColsPerStep * kUnroll) {
+      u32x2 c[kUnroll];
+#pragma unroll
+      for (int i = 0; i < kUnroll; ++i) {
+        const int64_t col = c0 + i * kColsPerStep + lane * 8;
+        c[i] = col < cols ? __builtin_nontemporal_load(cr + col / 8) : u32x2{0, 0};
+      }
+#pragma unroll
+      for (int i = 0; i < kUnroll; ++i) {
+        const int64_t col = c0 + i * kColsPerStep + lane * 8;
+        if (col < cols) {
+          const u32x4 h = {uncast2<false>(c[i].x), uncast2<true>(c[i].x),
+                           uncast2<false>(c[i].y), uncast2<true>(c[i].y)};
+          __builtin_nontemporal_store(h, hr + col / 8);
+        }
+      }
+    }
   }
 }
 
@@ -305,11 +435,23 @@ hipError_t decompress_code(const CodecBatch &b, int block, hipStream_t s) {
 }  // namespace
 
 hipError_t launch_compress(const CodecBatch &b, int code, int block, hipStream_t s) {
+  if (code == kCodeCast) {
+    const int grid = grid_for(b.row_begin[b.n]);
+    if (b.stats)
+      hipLaunchKernelGGL((cast_kernel<true>), dim3(grid), dim3(kThreads), 0, s, b);
+    else
+      hipLaunchKernelGGL((cast_kernel<false>), dim3(grid), dim3(kThreads), 0, s, b);
+    return hipGetLastError();
+  }
   return code == kCodeInt8 ? compress_code<kCodeInt8>(b, block, s)
                            : compress_code<kCodeE4M3>(b, block, s);
 }
 
 hipError_t launch_decompress(const CodecBatch &b, int code, int block, hipStream_t s) {
+  if (code == kCodeCast) {
+    hipLaunchKernelGGL(uncast_kernel, dim3(grid_for(b.row_begin[b.n])), dim3(kThreads), 0, s, b);
+    return hipGetLastError();
+  }
   return code == kCodeInt8 ? decompress_code<kCodeInt8>(b, block, s)
                            : decompress_code<kCodeE4M3>(b, block, s);
 }

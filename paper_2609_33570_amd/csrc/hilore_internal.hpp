@@ -9,6 +9,7 @@ namespace hilore {
 
 constexpr int kCodeInt8 = 0;
 constexpr int kCodeE4M3 = 1;
+constexpr int kCodeCast = 2;  // plain E4M3FN cast, no scales
 
 // One unit as the codec kernels see it (a validated copy of hilore_unit_desc).
 struct CodecUnit {

@@ -1,7 +1,9 @@
 // Weight gradient on a reconstructed L unit, dequantisation fused into the
 // tile load, on gfx950 MFMA:
 //   dW[i][j] (+)= sum_t xhat[t][i] * dY[t][j],
-//   xhat[t][i] = bf16_RNE(value(code[t][i]) * scale[t][i / BLOCK]).
+//   xhat[t][i] = bf16_RNE(value(code[t][i]) * scale[t][i / BLOCK]),
+// or, for the literal cast code (no scales), xhat[t][i] = value(code[t][i])
+// exactly.
 // This is the full-parameter weight gradient of a linear layer whose saved
 // input is kept in low precision (App. B.1; the full-parameter experiments of
 // App. D); gradients accumulate over microbatches (App. D.1.1).
@@ -119,15 +121,19 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t y_rsrc(const WgradArgs &a, int
                                            0x00020000);
 }
 
+template <int CODE>
 __device__ __forceinline__ void load_stage(Stage &st, const XRsrc &rs, const LoadPlan &lp) {
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
     st.xc[r] = __builtin_amdgcn_raw_buffer_load_b32(rs.x, (int)(lp.vo_x + r * lp.st_x), 0, 0);
-    st.xs[r] = __uint_as_float(
-        __builtin_amdgcn_raw_buffer_load_b32(rs.s, (int)(lp.vo_s + r * lp.st_s), 0, 0));
+    if constexpr (CODE != kCodeCast)
+      st.xs[r] = __uint_as_float(
+          __builtin_amdgcn_raw_buffer_load_b32(rs.s, (int)(lp.vo_s + r * lp.st_s), 0, 0));
   }
 }
-constexpr int kXLoads = 16;  // VMEM instructions issued by load_stage
+// VMEM instructions issued by load_stage (the literal cast has no scales)
+template <int CODE>
+constexpr int kXLoads = CODE == kCodeCast ? 8 : 16;
 
 typedef __attribute__((address_space(3))) void lds_void;
 
@@ -161,8 +167,13 @@ __device__ __forceinline__ void fill_x(const Stage &st, uint8_t *a_lds, int lc, 
 #pragma unroll
   for (int r = 0; r < 8; ++r) {
     const f32x2 q = decode_pair<CODE, C>(st.xc[r]);
-    lo[r] = q.x * st.xs[r];
-    hi[r] = q.y * st.xs[r];
+    if constexpr (CODE == kCodeCast) {  // exact bf16 values, no scale
+      lo[r] = q.x;
+      hi[r] = q.y;
+    } else {
+      lo[r] = q.x * st.xs[r];
+      hi[r] = q.y * st.xs[r];
+    }
   }
   u32x4 p;
   p.x = pack_bf16(lo[0], lo[1]);
@@ -281,14 +292,14 @@ __device__ __forceinline__ void region(f32x16 (&acc)[4][2], Frags &f, const uint
   if constexpr (KS == 2) fill_x<CODE, 0>(raw, nxt_a, lc, g);
   if constexpr (KS == 3) {
     fill_x<CODE, 2>(raw, nxt_a, lc, g);
-    load_stage(raw, rx, lp);
+    load_stage<CODE>(raw, rx, lp);
   }
   if constexpr (KS < 3) mma8_read<KS + 1>(acc, f, cur_a, cur_b, fp);
   if constexpr (KS == 3) mma8(acc, f);
   if constexpr (KS == 0) schedule_region<true, 0, 0, kYLoads>();
   if constexpr (KS == 1) schedule_region<true, 0, 0, 0>();
   if constexpr (KS == 2) schedule_region<true, 4, 2, 0>();
-  if constexpr (KS == 3) schedule_region<false, 4, 2, kXLoads>();
+  if constexpr (KS == 3) schedule_region<false, 4, 2, kXLoads<CODE>>();
 }
 
 // s_waitcnt with only the vector-memory count limited (expcnt and lgkmcnt
@@ -317,7 +328,7 @@ __device__ __forceinline__ void stage(f32x16 (&acc)[4][2], const uint8_t *cur_a,
   region<CODE, 1>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
   region<CODE, 2>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
   region<CODE, 3>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
-  wait_vmcnt<kXLoads>();
+  wait_vmcnt<kXLoads<CODE>>();
   __syncthreads();
 }
 
@@ -398,11 +409,11 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_kernel(const WgradArgs a, i
   const int64_t n_stages = ((a.K + BK - 1) / BK + 1) & ~int64_t(1);
   Stage raw;
   dma_dy(y_rsrc(a, 0), lp, lds_b0, wave);
-  load_stage(raw, x_rsrc<BLOCK>(a, 0), lp);
+  load_stage<CODE>(raw, x_rsrc<BLOCK>(a, 0), lp);
   fill_x<CODE, 0>(raw, lds_a0, lc, g);
   fill_x<CODE, 2>(raw, lds_a0, lc, g);
-  load_stage(raw, x_rsrc<BLOCK>(a, BK), lp);
-  wait_vmcnt<kXLoads>();
+  load_stage<CODE>(raw, x_rsrc<BLOCK>(a, BK), lp);
+  wait_vmcnt<kXLoads<CODE>>();
   __syncthreads();
 
   for (int64_t s = 0; s < n_stages; s += 2) {
@@ -431,24 +442,30 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_kernel(const WgradArgs a, i
   }
 }
 
-template <int CODE>
-hipError_t dispatch(const WgradArgs &a, int block, hipStream_t s) {
+template <int CODE, int BLOCK>
+hipError_t launch_one(const WgradArgs &a, hipStream_t s) {
   const int tiles_m = (int)((a.M + BM - 1) / BM);
   const int tiles_n = (int)((a.N + BN - 1) / BN);
-  const dim3 grid(tiles_m * tiles_n);
-  switch (block) {
-    case 32: hipLaunchKernelGGL((wgrad_kernel<CODE, 32>), grid, dim3(kThreads), 0, s, a, tiles_m, tiles_n); break;
-    case 64: hipLaunchKernelGGL((wgrad_kernel<CODE, 64>), grid, dim3(kThreads), 0, s, a, tiles_m, tiles_n); break;
-    case 128: hipLaunchKernelGGL((wgrad_kernel<CODE, 128>), grid, dim3(kThreads), 0, s, a, tiles_m, tiles_n); break;
-    default: hipLaunchKernelGGL((wgrad_kernel<CODE, 256>), grid, dim3(kThreads), 0, s, a, tiles_m, tiles_n); break;
-  }
+  hipLaunchKernelGGL((wgrad_kernel<CODE, BLOCK>), dim3(tiles_m * tiles_n), dim3(kThreads), 0, s,
+                     a, tiles_m, tiles_n);
   return hipGetLastError();
+}
+
+template <int CODE>
+hipError_t dispatch(const WgradArgs &a, int block, hipStream_t s) {
+  switch (block) {
+    case 32: return launch_one<CODE, 32>(a, s);
+    case 64: return launch_one<CODE, 64>(a, s);
+    case 128: return launch_one<CODE, 128>(a, s);
+    default: return launch_one<CODE, 256>(a, s);
+  }
 }
 
 }  // namespace
 
 hipError_t launch_wgrad(const WgradArgs &a, int code, int block, hipStream_t s) {
   if (a.M == 0 || a.N == 0) return hipSuccess;
+  if (code == kCodeCast) return launch_one<kCodeCast, 256>(a, s);  // no blocks; BLOCK unused
   return code == kCodeInt8 ? dispatch<kCodeInt8>(a, block, s) : dispatch<kCodeE4M3>(a, block, s);
 }
 

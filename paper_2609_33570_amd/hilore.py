@@ -23,7 +23,9 @@ HILORE_ERR_HIP = 5
 
 HILORE_CODE_INT8 = 0
 HILORE_CODE_FP8_E4M3FN = 1
-CODES = {"int8": HILORE_CODE_INT8, "e4m3fn": HILORE_CODE_FP8_E4M3FN}
+HILORE_CODE_FP8_E4M3FN_CAST = 2  # the paper's literal codec: plain cast, no scales, block 0
+CODES = {"int8": HILORE_CODE_INT8, "e4m3fn": HILORE_CODE_FP8_E4M3FN,
+         "e4m3fn_cast": HILORE_CODE_FP8_E4M3FN_CAST}
 
 
 class HiloreError(RuntimeError):

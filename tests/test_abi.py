@@ -92,7 +92,11 @@ def codec(lib, fn, units, code=0, block=128):
 @pytest.mark.parametrize("fn", ["hilore_compress", "hilore_decompress"])
 def test_codec_validation(lib, fn):
     E = hilore
+    assert codec(lib, fn, [unit()], code=3) == E.HILORE_ERR_INVALID_ARG
+    # the literal cast has no blocks: block must be 0, and scales are not needed
     assert codec(lib, fn, [unit()], code=2) == E.HILORE_ERR_INVALID_ARG
+    assert codec(lib, fn, [unit(scales=None, codes=FAKE + 1)], code=2, block=0) == E.HILORE_ERR_ALIGNMENT
+    assert codec(lib, fn, [unit(scales=None, codes=None)], code=2, block=0) == E.HILORE_ERR_INVALID_ARG
     assert codec(lib, fn, [unit()], block=48) == E.HILORE_ERR_UNSUPPORTED
     assert codec(lib, fn, [unit()], block=512) == E.HILORE_ERR_UNSUPPORTED
     assert codec(lib, fn, [unit(cols=200)], block=128) == E.HILORE_ERR_UNSUPPORTED
@@ -162,3 +166,8 @@ def test_wgrad_validation(lib):
     assert wgrad(lib, dy=None) == E.HILORE_ERR_INVALID_ARG
     assert wgrad(lib, x_scales=FAKE + 4) == E.HILORE_ERR_ALIGNMENT
     assert wgrad(lib, M=0) == E.HILORE_OK
+    # the literal cast: block 0 only, no M % block rule, scales may be NULL
+    assert wgrad(lib, code=2) == E.HILORE_ERR_INVALID_ARG
+    assert wgrad(lib, code=2, block=0, N=100) == E.HILORE_ERR_UNSUPPORTED
+    assert wgrad(lib, code=2, block=0, x_scales=None, x_codes=FAKE + 1) == E.HILORE_ERR_ALIGNMENT
+    assert wgrad(lib, code=2, block=0, x_scales=None, dy=None) == E.HILORE_ERR_INVALID_ARG

@@ -158,3 +158,75 @@ def test_deterministic(hl, orc):
     r2 = gpu_codec(hl, xs, 1, 128)[0]
     for a, b in zip(r1, r2):
         assert_bytes_equal(a, b, "repeat")
+
+
+# --- the paper's literal codec: plain E4M3FN cast, no scales ---------------
+
+CAST = 2
+
+
+def gpu_cast(hl, xs, stats=True, cols=None):
+    units_c, units_d, bufs = [], [], []
+    for i, x in enumerate(xs):
+        rows, ld = x.shape
+        c = ld if cols is None else cols[i]
+        xd = dev(x)
+        codes = filled((rows, c), torch.uint8, 0xEE)
+        xhat = filled((rows, c), torch.int16, 0x1234)
+        ssx = filled((rows,), torch.float32, -1.0) if stats else None
+        sse = filled((rows,), torch.float32, -1.0) if stats else None
+        bufs.append((xd, codes, xhat, ssx, sse))  # xd too: the inputs must outlive the call
+        units_c.append(hl.unit_desc(x=xd, codes=codes, row_ss_x=ssx, row_ss_err=sse, rows=rows,
+                                    cols=c, ld=ld))
+        units_d.append(hl.unit_desc(codes=codes, xhat=xhat, rows=rows, cols=c))
+    hl.hilore_compress(units_c, CAST, 0)
+    hl.hilore_decompress(units_d, CAST, 0)
+    torch.cuda.synchronize()
+    return [(host(c), host(h).view(np.uint16), host(a) if stats else None,
+             host(b) if stats else None) for _, c, h, a, b in bufs]
+
+
+def check_cast(orc, x, res, cols=None, what=""):
+    codes, xhat, ssx, sse = res
+    o_codes, o_scales = orc.quantize(x, CAST, 0, cols=cols)
+    assert o_scales is None
+    o_xhat = orc.dequantize(o_codes, None, CAST, 0)
+    assert_bytes_equal(codes, o_codes, f"{what} codes")
+    assert_bytes_equal(xhat, o_xhat, f"{what} xhat")
+    if ssx is not None:
+        c = o_codes.shape[1]
+        o_ssx, o_sse = orc.row_stats(np.ascontiguousarray(x[:, :c]), o_xhat)
+        for name, g, o in (("x^2", ssx, o_ssx), ("err^2", sse, o_sse)):
+            nan = np.isnan(o)
+            assert np.array_equal(np.isnan(g), nan), f"{what} row sum {name} NaN rows"
+            fits = ~nan & (o < 1e38)
+            assert_close(g[fits], o[fits], f"{what} row sum {name}")
+            assert (g[~nan & ~fits] >= 1e38).all(), f"{what} row sum {name} past fp32 range"
+
+
+def test_cast_every_bf16_pattern(hl, orc):
+    """All 65536 bf16 bit patterns (finite, infinite, NaN) as one 256 x 256
+    unit: codes and the cast back bit for bit."""
+    x = np.arange(1 << 16, dtype=np.uint32).astype(np.uint16).reshape(256, 256)
+    (res,) = gpu_cast(hl, [x], stats=False)
+    check_cast(orc, x, res, what="all bf16")
+
+
+def test_cast_activations_with_overflow(hl, orc):
+    """Activations whose outlier channels pass the E4M3FN range (NaN codes),
+    with the per-row sums, ragged rows and several units per call."""
+    xs = []
+    for i, (r, c) in enumerate([(300, 3584), (37, 520), (5, 8), (64, 18944)]):
+        x = wl.activation_host(r, c, seed=300 + i, outliers=("channels", 0.01, 30.0))
+        xf = (x.astype(np.uint32) << 16).view(np.float32) * np.float32(20.0)  # push outliers past 464
+        xs.append(wl.to_bf16_bits(xf))
+    res = gpu_cast(hl, xs)
+    for i, (x, r) in enumerate(zip(xs, res)):
+        check_cast(orc, x, r, what=f"unit {i}")
+    assert ((res[0][0] & 0x7F) == 0x7F).any(), "the test should produce NaN codes"
+
+
+def test_cast_strided_rows(hl, orc):
+    x = wl.activation_host(50, 768, seed=7, ld=1024)
+    (res,) = gpu_cast(hl, [x], cols=[768])
+    check_cast(orc, x, res, cols=768, what="strided")

@@ -98,3 +98,29 @@ def test_deterministic(hl, orc):
     a = gpu_wgrad(hl, codes, scales, 1, 128, dy)
     b = gpu_wgrad(hl, codes, scales, 1, 128, dy)
     assert_bytes_equal(a, b, "repeat")
+
+
+def test_literal_cast_integer_exact(hl, orc):
+    """Literal cast codes (no scales) of small integers: exact in any order."""
+    g = np.random.default_rng(15)
+    K, M, N = 4096, 256, 264
+    xi = g.integers(-8, 9, size=(K, M)).astype(np.float32)
+    codes, _ = orc.quantize(wl.to_bf16_bits(xi), 2, 0)
+    dy = wl.to_bf16_bits(g.integers(-8, 9, size=(K, N)).astype(np.float32))
+    dw = filled((M, N), torch.float32, float("nan"))
+    hl.hilore_dequant_wgrad(dev(codes), None, 2, 0, dev(dy), dw, K, M, N, False)
+    torch.cuda.synchronize()
+    want = orc.wgrad(codes, None, 2, 0, dy, variant=1)
+    assert_bytes_equal(host(dw), want.astype(np.float32), "dW")
+
+
+def test_literal_cast_activations(hl, orc):
+    K, M, N = 1000, 512, 264
+    x = wl.activation_host(K, M, seed=16, outliers=("channels", 0.01, 30.0))
+    codes, _ = orc.quantize(x, 2, 0)
+    assert not ((codes & 0x7F) == 0x7F).any()
+    dy = wl.normal_bf16_host(K, N, seed=17, sigma=0.02)
+    dw = filled((M, N), torch.float32, float("nan"))
+    hl.hilore_dequant_wgrad(dev(codes), None, 2, 0, dev(dy), dw, K, M, N, False)
+    torch.cuda.synchronize()
+    assert rel_fro(host(dw), orc.wgrad(codes, None, 2, 0, dy, variant=1)) <= 1e-5

@@ -103,3 +103,61 @@ def test_code_values(orc):
     assert orc.code_value(orc.E4M3FN, 0x7E) == 448.0
     assert orc.code_value(orc.E4M3FN, 0x01) == 2.0 ** -9
     assert orc.code_value(orc.E4M3FN, 0x08) == 2.0 ** -6
+
+
+# --- the paper's literal codec: a plain torch.float8_e4m3fn cast (App. B.1,
+# Eq. fp8-roundtrip, "without scales, zero-points, or outlier tensors") -------
+
+def test_e4m3_cast_matches_torch_on_every_bf16(orc):
+    """The cast of every bf16 bit pattern (finite, infinite and NaN) equals
+    torch's own CPU cast byte for byte, overflow-to-NaN included."""
+    bits = (np.arange(1 << 16, dtype=np.uint32) << 16)
+    v = _f32(bits)
+    ref = torch.from_numpy(bits.astype(np.uint32).view(np.int32) >> 16).to(torch.int16)
+    ref = ref.view(torch.bfloat16).to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(orc.e4m3fn_cast(v), ref)
+
+
+def test_e4m3_cast_matches_torch_random_fp32(orc):
+    g = np.random.default_rng(12)
+    bits = g.integers(0, 1 << 32, size=1 << 20, dtype=np.uint64).astype(np.uint32)
+    # concentrate half of the samples on the E4M3FN range and its overflow edge
+    mags = g.uniform(0, 520, size=1 << 19).astype(np.float32) * np.where(g.random(1 << 19) < .5, -1, 1)
+    v = np.concatenate([_f32(bits), mags.astype(np.float32)])
+    assert np.array_equal(orc.e4m3fn_cast(v), _torch_e4m3_bits(v))
+
+
+def test_e4m3_cast_overflow_edge(orc):
+    # 464 is the midpoint of 448 and the would-be 480: ties to even -> 448;
+    # anything past it has no encoding -> NaN with the sign kept
+    v = np.float32([448.0, 463.99997, 464.0, np.nextafter(np.float32(464), np.float32(1e9)),
+                    -464.0, -465.0, np.inf, -np.inf, -0.0])
+    assert orc.e4m3fn_cast(v).tolist() == [0x7E, 0x7E, 0x7E, 0x7F, 0xFE, 0xFF, 0x7F, 0xFF, 0x80]
+
+
+def test_e4m3_cast_back_matches_torch(orc):
+    codes = torch.arange(256, dtype=torch.int32).to(torch.uint8)
+    ref = codes.view(torch.float8_e4m3fn).to(torch.bfloat16).view(torch.int16).numpy()
+    ref = ref.view(np.uint16)
+    ours = np.array([orc.e4m3fn_cast_to_bf16(c) for c in range(256)], dtype=np.uint16)
+    assert np.array_equal(ours, ref)
+    assert ours[0x7F] == ours[0xFF] == 0x7FC0
+
+
+def test_literal_codec_roundtrip_is_torch_roundtrip(orc):
+    """quantize/dequantize with the literal code reproduce
+    x.to(float8_e4m3fn).to(bfloat16) of torch on a tensor with overflow."""
+    g = np.random.default_rng(13)
+    x = (g.standard_normal((37, 96)) * 120).astype(np.float32)
+    x[3, 5] = 600.0
+    x[7, 9] = -1e30
+    xb = torch.from_numpy(x).to(torch.bfloat16)
+    xu = xb.view(torch.int16).numpy().view(np.uint16)
+    codes, scales = orc.quantize(xu, orc.E4M3FN_CAST, 0)
+    assert scales is None
+    ref_c = xb.to(torch.float8_e4m3fn).view(torch.uint8).numpy()
+    assert np.array_equal(codes, ref_c)
+    xh = orc.dequantize(codes, None, orc.E4M3FN_CAST, 0)
+    ref_h = xb.to(torch.float8_e4m3fn).to(torch.bfloat16).view(torch.int16).numpy().view(np.uint16)
+    assert np.array_equal(xh, ref_h)
+    assert xh[3, 5] == 0x7FC0 and xh[7, 9] == 0x7FC0

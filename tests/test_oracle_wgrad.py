@@ -63,3 +63,19 @@ def test_ones_column_gives_column_sums(orc):
     xh = f32(orc.dequantize(codes, scales, orc.E4M3FN, 32)).astype(np.float64)
     np.testing.assert_allclose(dw[:, 3], xh.sum(axis=0), rtol=1e-14)
     assert (dw[:, np.arange(N) != 3] == 0).all()
+
+
+def test_literal_cast_code_matches_torch_cast_operand(orc):
+    """With the literal codec the operand is torch's own bf16 -> float8_e4m3fn
+    -> bf16 round trip; the oracle's wgrad equals numpy on it."""
+    import torch
+    K, M, N = 80, 64, 40
+    x = wl.activation_host(K, M, seed=34, outliers=("channels", 0.05, 30.0))
+    xt = torch.from_numpy(x.view(np.int16)).view(torch.bfloat16)
+    xh = xt.to(torch.float8_e4m3fn).to(torch.float32).numpy().astype(np.float64)
+    codes, scales = orc.quantize(x, orc.E4M3FN_CAST, 0)
+    dy = wl.normal_bf16_host(K, N, seed=35, sigma=0.02)
+    ref = xh.T @ f32(dy).astype(np.float64)
+    for variant in (0, 1):
+        dw = orc.wgrad(codes, None, orc.E4M3FN_CAST, 0, dy, variant=variant)
+        np.testing.assert_allclose(dw, ref, rtol=1e-12, atol=1e-14 * np.abs(ref).max())
