@@ -72,6 +72,8 @@ def lib() -> ctypes.CDLL:
             "orc_unit_exposure_risk": (None, [P, P, i64, P, P, i64, f64, f64, P, P, P]),
             "orc_wgrad": (None, [P, P, i32, i32, P, i64, i64, i64, i64, i64, i64, i64, i32, P]),
             "orc_wgrad_entries": (None, [P, P, i32, i32, P, i64, i64, i64, P, P, i64, i32, P]),
+            "orc_allocate": (i32, [i32, P, P, P, P, P, P, P, f64, f64, i32, i32, P, P, P]),
+            "orc_allocate_brute": (i32, [i32, P, P, P, P, P, P, P, f64, f64, i32, i32, P, P, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -241,3 +243,27 @@ def wgrad_entries(codes, scales, code, block, dy_u16, ii, jj, variant=0, K=None)
     lib().orc_wgrad_entries(_ptr(c), _ptr(s), code, block, _ptr(d), Kc if K is None else K, M,
                             N, _ptr(ii), _ptr(jj), ii.size, variant, _ptr(out))
     return out
+
+
+# ------------------------------------------------------------- allocation --
+ACT_R, ACT_H, ACT_L = 0, 1, 2
+
+
+def allocate(q, verified, tau_h, tau_l, dm_h, dm_l, psi, m_res, delta_b, n_b=1024, n_d=1024,
+             brute=False):
+    """Joint H/L/R allocation of App. B.2 (dynamic programme, or brute force
+    over 3^U with brute=True).  Returns (action u8[U], totals f64[3] =
+    (utility, memory, risk), jk i64[2] = terminal integer costs)."""
+    q = _c(q, np.uint8)
+    v = _c(verified, np.uint8)
+    arrs = [_c(a, np.float64) for a in (tau_h, tau_l, dm_h, dm_l, psi)]
+    U = q.size
+    action = np.zeros(max(U, 1), dtype=np.uint8)
+    totals = np.zeros(3, dtype=np.float64)
+    jk = np.zeros(2, dtype=np.int64)
+    fn = lib().orc_allocate_brute if brute else lib().orc_allocate
+    rc = fn(U, _ptr(q), _ptr(v), *[_ptr(a) for a in arrs], float(m_res), float(delta_b),
+            int(n_b), int(n_d), _ptr(action), _ptr(totals), _ptr(jk))
+    if rc != 0:
+        raise ValueError("invalid allocation arguments")
+    return action[:U], totals, jk

@@ -437,3 +437,205 @@ void orc_wgrad_entries(const uint8_t *codes, const float *scales, int code, int 
     out[e] = acc;
   }
 }
+
+/* ======================================================================= */
+/* Recovery allocation                                                     */
+/* ======================================================================= */
+
+/* Sec. 3.4 Eq. joint-allocation, solved as in App. B.2: each unit u takes one
+ * action a in A_u(q_u) from {R, H, L}; R is the baseline with zero utility,
+ * memory and risk; H has risk 0; L has risk psi_u.  Maximise the summed
+ * utility subject to  sum dm <= m_res  and  sum risk <= delta_b.
+ *
+ * Available actions (App. B.3 Eq. available-recovery-actions): the verified
+ * set of the unit intersected with {H,L,R} if the retained representation q_u
+ * is H, {L,R} if it is L, {R} if it is R.  Non-R actions with non-positive
+ * utility are excluded (App. B.2, utility profiling); so are actions whose
+ * inputs are not finite or negative.  A zero risk budget disables L; a zero
+ * memory budget admits only actions with zero memory cost. */
+static int action_ok(int act, uint8_t q, uint8_t verified, double tau, double dm, double risk) {
+  if (!((verified >> act) & 1u)) return 0;
+  if (q == ORC_ACT_L && act == ORC_ACT_H) return 0;  /* an L copy cannot give H */
+  if (q != ORC_ACT_H && q != ORC_ACT_L) return 0;    /* R (or unknown): only R */
+  if (!(tau > 0.0) || !isfinite(tau)) return 0;
+  if (!(dm >= 0.0) || !isfinite(dm)) return 0;
+  if (!(risk >= 0.0) || !isfinite(risk)) return 0;
+  return 1;
+}
+
+/* Integer cost of one action on a grid of n intervals of width h (Eq.
+ * allocation-integer-costs): ceil(cost / h), or n + 1 (does not fit) when
+ * that exceeds n.  With a zero budget (h unused) only a zero cost fits. */
+static int64_t grid_cost(double cost, double budget, int n) {
+  if (!(budget > 0.0)) return cost == 0.0 ? 0 : (int64_t)n + 1;
+  const double h = budget / (double)n;
+  const double c = ceil(cost / h);
+  return c > (double)n ? (int64_t)n + 1 : (int64_t)c;
+}
+
+typedef struct {
+  int ok_h, ok_l;
+  int64_t b_h, b_l, r_l;
+  double tau_h, tau_l;
+} unit_costs;
+
+static void costs_of(int u, const uint8_t *q, const uint8_t *verified, const double *tau_h,
+                     const double *tau_l, const double *dm_h, const double *dm_l,
+                     const double *psi, double m_res, double delta_b, int n_b, int n_d,
+                     unit_costs *c) {
+  c->ok_h = action_ok(ORC_ACT_H, q[u], verified[u], tau_h[u], dm_h[u], 0.0);
+  c->ok_l = action_ok(ORC_ACT_L, q[u], verified[u], tau_l[u], dm_l[u], psi[u]) && delta_b > 0.0;
+  c->b_h = c->ok_h ? grid_cost(dm_h[u], m_res, n_b) : 0;
+  c->b_l = c->ok_l ? grid_cost(dm_l[u], m_res, n_b) : 0;
+  c->r_l = c->ok_l ? grid_cost(psi[u], delta_b, n_d) : 0;
+  if (c->b_h > n_b) c->ok_h = 0;
+  if (c->b_l > n_b || c->r_l > n_d) c->ok_l = 0;
+  c->tau_h = tau_h[u];
+  c->tau_l = tau_l[u];
+}
+
+/* Grid sizes of Eq. allocation-grid: N + 1 states per axis, or a single state
+ * when the budget on that axis is zero. */
+static void grid_sizes(double m_res, double delta_b, int n_b, int n_d, int64_t *KB, int64_t *KD) {
+  *KB = m_res > 0.0 ? (int64_t)n_b + 1 : 1;
+  *KD = delta_b > 0.0 ? (int64_t)n_d + 1 : 1;
+}
+
+/* The dynamic programme of Eq. allocation-dp: F_i(j, k) is the largest
+ * utility of units 1..i with integer memory cost exactly j and risk cost
+ * exactly k; F_0(0,0) = 0, every other F_0 entry -inf;
+ *   F_i(j,k) = max over available a with b_i(a) <= j, r_i(a) <= k of
+ *              F_{i-1}(j - b_i(a), k - r_i(a)) + utility_i(a),
+ * actions tried in the order R, H, L and replaced only by a strictly larger
+ * value (the within-state tie rule).  The answer is the best terminal state,
+ * ties to lower risk, then lower memory; the actions are recovered by
+ * backtracking.  Outputs: action[u] in {0 = R, 1 = H, 2 = L}; totals = {summed
+ * utility, memory, risk} (sums in unit order); jk = the terminal integer costs.
+ * Returns 0, or -1 on invalid scalars. */
+int orc_allocate(int U, const uint8_t *q, const uint8_t *verified, const double *tau_h,
+                 const double *tau_l, const double *dm_h, const double *dm_l, const double *psi,
+                 double m_res, double delta_b, int n_b, int n_d, uint8_t *action,
+                 double *totals, int64_t *jk) {
+  if (U < 0 || n_b < 1 || n_d < 1 || !(m_res >= 0.0) || !isfinite(m_res) ||
+      !(delta_b >= 0.0) || !isfinite(delta_b))
+    return -1;
+  int64_t KB, KD;
+  grid_sizes(m_res, delta_b, n_b, n_d, &KB, &KD);
+  const int64_t cells = KB * KD;
+  double *prev = (double *)malloc(sizeof(double) * (size_t)cells);
+  double *cur = (double *)malloc(sizeof(double) * (size_t)cells);
+  uint8_t *pred = (uint8_t *)malloc((size_t)(U > 0 ? U : 1) * (size_t)cells);
+  unit_costs *uc = (unit_costs *)malloc(sizeof(unit_costs) * (size_t)(U > 0 ? U : 1));
+  for (int64_t c = 0; c < cells; ++c) prev[c] = -INFINITY;
+  prev[0] = 0.0;                                  /* F_0(0,0) = 0, cell index k * KB + j */
+  for (int i = 0; i < U; ++i) {
+    costs_of(i, q, verified, tau_h, tau_l, dm_h, dm_l, psi, m_res, delta_b, n_b, n_d, &uc[i]);
+    const unit_costs *c = &uc[i];
+    for (int64_t k = 0; k < KD; ++k)
+      for (int64_t j = 0; j < KB; ++j) {
+        double best = prev[k * KB + j];           /* R */
+        uint8_t a = ORC_ACT_R;
+        if (c->ok_h && c->b_h <= j) {
+          const double v = prev[k * KB + (j - c->b_h)] + c->tau_h;
+          if (v > best) { best = v; a = ORC_ACT_H; }
+        }
+        if (c->ok_l && c->b_l <= j && c->r_l <= k) {
+          const double v = prev[(k - c->r_l) * KB + (j - c->b_l)] + c->tau_l;
+          if (v > best) { best = v; a = ORC_ACT_L; }
+        }
+        cur[k * KB + j] = best;
+        pred[(int64_t)i * cells + k * KB + j] = a;
+      }
+    double *t = prev; prev = cur; cur = t;
+  }
+  /* best terminal state: scanning risk, then memory, upward keeps the first */
+  int64_t bj = 0, bk = 0;
+  double bv = prev[0];
+  for (int64_t k = 0; k < KD; ++k)
+    for (int64_t j = 0; j < KB; ++j)
+      if (prev[k * KB + j] > bv) { bv = prev[k * KB + j]; bj = j; bk = k; }
+  jk[0] = bj;
+  jk[1] = bk;
+  totals[0] = bv;
+  int64_t j = bj, k = bk;
+  for (int i = U - 1; i >= 0; --i) {
+    const uint8_t a = pred[(int64_t)i * cells + k * KB + j];
+    action[i] = a;
+    if (a == ORC_ACT_H) j -= uc[i].b_h;
+    if (a == ORC_ACT_L) { j -= uc[i].b_l; k -= uc[i].r_l; }
+  }
+  double mem = 0.0, risk = 0.0;
+  for (int i = 0; i < U; ++i) {
+    if (action[i] == ORC_ACT_H) mem += dm_h[i];
+    if (action[i] == ORC_ACT_L) { mem += dm_l[i]; risk += psi[i]; }
+  }
+  totals[1] = mem;
+  totals[2] = risk;
+  free(prev); free(cur); free(pred); free(uc);
+  return 0;
+}
+
+/* Brute force over all 3^U assignments of the same discretised problem
+ * (U <= 16): the utility of an assignment is its non-R utilities added in
+ * unit order; feasible when every action is available and the integer costs
+ * sum to at most n_b and n_d.  Best value first, then lower risk cost, then
+ * lower memory cost, then the assignment that is smallest when compared from
+ * the last unit backwards (R < H < L).  Same outputs as orc_allocate. */
+int orc_allocate_brute(int U, const uint8_t *q, const uint8_t *verified, const double *tau_h,
+                       const double *tau_l, const double *dm_h, const double *dm_l,
+                       const double *psi, double m_res, double delta_b, int n_b, int n_d,
+                       uint8_t *action, double *totals, int64_t *jk) {
+  if (U < 0 || U > 16 || n_b < 1 || n_d < 1 || !(m_res >= 0.0) || !isfinite(m_res) ||
+      !(delta_b >= 0.0) || !isfinite(delta_b))
+    return -1;
+  unit_costs uc[16];
+  for (int i = 0; i < U; ++i)
+    costs_of(i, q, verified, tau_h, tau_l, dm_h, dm_l, psi, m_res, delta_b, n_b, n_d, &uc[i]);
+  int64_t total = 1;
+  for (int i = 0; i < U; ++i) total *= 3;
+  int have = 0;
+  double bv = 0.0;
+  int64_t bj = 0, bk = 0;
+  uint8_t best[16] = {0}, a[16];
+  for (int64_t code = 0; code < total; ++code) {
+    int64_t x = code, j = 0, k = 0;
+    double v = 0.0;
+    int ok = 1;
+    for (int i = 0; i < U; ++i) {
+      a[i] = (uint8_t)(x % 3);
+      x /= 3;
+      if (a[i] == ORC_ACT_H) {
+        if (!uc[i].ok_h) { ok = 0; break; }
+        j += uc[i].b_h;
+        v += uc[i].tau_h;
+      } else if (a[i] == ORC_ACT_L) {
+        if (!uc[i].ok_l) { ok = 0; break; }
+        j += uc[i].b_l;
+        k += uc[i].r_l;
+        v += uc[i].tau_l;
+      }
+    }
+    if (!ok || j > n_b || k > n_d) continue;
+    int better = !have || v > bv || (v == bv && (k < bk || (k == bk && j < bj)));
+    if (!better && v == bv && k == bk && j == bj) {
+      for (int i = U - 1; i >= 0; --i)
+        if (a[i] != best[i]) { better = a[i] < best[i]; break; }
+    }
+    if (better) {
+      have = 1; bv = v; bj = j; bk = k;
+      memcpy(best, a, (size_t)U);
+    }
+  }
+  memcpy(action, best, (size_t)U);
+  jk[0] = bj;
+  jk[1] = bk;
+  totals[0] = bv;
+  double mem = 0.0, risk = 0.0;
+  for (int i = 0; i < U; ++i) {
+    if (action[i] == ORC_ACT_H) mem += dm_h[i];
+    if (action[i] == ORC_ACT_L) { mem += dm_l[i]; risk += psi[i]; }
+  }
+  totals[1] = mem;
+  totals[2] = risk;
+  return 0;
+}

@@ -89,6 +89,24 @@ void orc_wgrad_entries(const uint8_t *codes, const float *scales, int code, int 
                        const int64_t *ii, const int64_t *jj, int64_t n, int variant,
                        double *out);
 
+/* ---- recovery allocation (Sec. 3.4 Eq. joint-allocation; App. B.2 Eqs.
+ *      allocation-grid, allocation-integer-costs, allocation-dp; App. B.3 Eq.
+ *      available-recovery-actions).  Per unit: q = retained representation and
+ *      action ids 0 = R, 1 = H, 2 = L; verified = bit mask of verified actions;
+ *      tau_* utilities, dm_* memory costs, psi the risk of L.  m_res and delta_b
+ *      are the memory and risk budgets, n_b and n_d the grid intervals (1024 in
+ *      the paper).  Returns 0, or -1 on invalid scalars. */
+enum { ORC_ACT_R = 0, ORC_ACT_H = 1, ORC_ACT_L = 2 };
+int orc_allocate(int U, const uint8_t *q, const uint8_t *verified, const double *tau_h,
+                 const double *tau_l, const double *dm_h, const double *dm_l, const double *psi,
+                 double m_res, double delta_b, int n_b, int n_d, uint8_t *action,
+                 double *totals, int64_t *jk);
+/* the same problem by enumerating all 3^U assignments (U <= 16) */
+int orc_allocate_brute(int U, const uint8_t *q, const uint8_t *verified, const double *tau_h,
+                       const double *tau_l, const double *dm_h, const double *dm_l,
+                       const double *psi, double m_res, double delta_b, int n_b, int n_d,
+                       uint8_t *action, double *totals, int64_t *jk);
+
 #ifdef __cplusplus
 }
 #endif

@@ -257,3 +257,80 @@ def plan_actions(n_units: int, seed: int, frac_l: float = 0.4, frac_h: float = 0
     act[perm[:n_l]] = "L"
     act[perm[n_l:n_l + n_h]] = "H"
     return act
+
+
+# ------------------------------------------------------ allocation instances --
+@dataclasses.dataclass
+class AllocInstance:
+    """Inputs of one H/L/R allocation (App. B.2): per unit the retained
+    representation q (0 = R, 1 = H, 2 = L), the verified-action bit mask
+    (bit a for action a), the utilities and memory costs of H and L, and the
+    risk psi of L; the memory and risk budgets of the microbatch."""
+    q: np.ndarray
+    verified: np.ndarray
+    tau_h: np.ndarray
+    tau_l: np.ndarray
+    dm_h: np.ndarray
+    dm_l: np.ndarray
+    psi: np.ndarray
+    m_res: float
+    delta_b: float
+
+    @property
+    def U(self) -> int:
+        return int(self.q.size)
+
+    def arrays(self):
+        return (self.q, self.verified, self.tau_h, self.tau_l, self.dm_h, self.dm_l, self.psi)
+
+
+def alloc_instance(shapes: Sequence[Tuple[int, int]], seed: int, block: int = 128,
+                   frac_q: Tuple[float, float, float] = (0.15, 0.6, 0.25),
+                   mem_frac: float = 0.3, risk_frac: float = 0.25) -> AllocInstance:
+    """Synthetic profiled units of the given (rows, cols) bf16 shapes.  H keeps
+    the tensor (2 B per element), L its codes and scales (1 + 4/block B); the
+    H utility is the recompute time saved, drawn around the time to stream the
+    tensor at 1.5 TB/s (x U(0.6, 1.6)); L saves the same minus a codec cost of
+    3 B per element at 5 TB/s (x U(0.8, 1.2)), so a few L utilities are not
+    positive; psi ~ lognormal(-7, 1.5).  q is R/H/L with probabilities frac_q;
+    10% of the units lack a verified L.  Budgets: mem_frac of the total H
+    memory and risk_frac of the total psi."""
+    g = rng(seed, 6)
+    U = len(shapes)
+    n = np.array([r * c for r, c in shapes], dtype=np.float64)
+    dm_h = 2.0 * n
+    dm_l = n * (1.0 + 4.0 / block)
+    tau_h = dm_h / 1.5e12 * g.uniform(0.6, 1.6, U)
+    tau_l = tau_h - 3.0 * n / 5e12 * g.uniform(0.8, 1.2, U)
+    psi = g.lognormal(-7.0, 1.5, U)
+    q = g.choice(3, size=U, p=np.asarray(frac_q) / np.sum(frac_q)).astype(np.uint8)
+    verified = np.where(g.random(U) < 0.1, 0b011, 0b111).astype(np.uint8)
+    return AllocInstance(q, verified, tau_h, tau_l, dm_h, dm_l, psi,
+                         float(mem_frac * dm_h.sum()), float(risk_frac * psi.sum()))
+
+
+def alloc_small(U: int, seed: int, integer: bool = False, scale: float = 16.0) -> AllocInstance:
+    """Small random instance for exhaustive checks: memory costs and psi of a
+    few grid steps (so that budgets bind), utilities real or small integers
+    (integers make many exact ties)."""
+    g = rng(seed, 7)
+    if integer:
+        tau_h = g.integers(1, 4, U).astype(np.float64)
+        tau_l = g.integers(0, 4, U).astype(np.float64)
+    else:
+        tau_h = g.uniform(0.1, 2.0, U)
+        tau_l = g.uniform(-0.2, 2.0, U)
+    dm_h = g.uniform(0.0, scale, U) * (g.random(U) < 0.9)
+    dm_l = dm_h * g.uniform(0.3, 0.7, U)
+    psi = g.uniform(0.0, scale, U) * (g.random(U) < 0.9)
+    q = g.choice(3, size=U, p=[0.2, 0.55, 0.25]).astype(np.uint8)
+    verified = np.where(g.random(U) < 0.15, 0b011, 0b111).astype(np.uint8)
+    return AllocInstance(q, verified, tau_h, tau_l, dm_h, dm_l, psi,
+                         float(g.uniform(0.2, 0.6) * dm_h.sum()),
+                         float(g.uniform(0.2, 0.6) * psi.sum()))
+
+
+def qwen2_7b_unit_mix(layers: int = 28, tokens: int = 16384) -> Tuple[Tuple[int, int], ...]:
+    """Per decoder layer 4 hidden-width (3584) and 3 MLP-width (18944) saved
+    activations of the microbatch: 196 units for 28 layers."""
+    return tuple((tokens, c) for _ in range(layers) for c in (3584,) * 4 + (18944,) * 3)
