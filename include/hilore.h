@@ -147,7 +147,7 @@ hilore_status hilore_grpo_coeffs(const float *rewards, const float *logp_new,
  * cast back (a NaN code makes its row's ss_err NaN).
  * All units of one call are encoded on `stream`; they may differ in shape.
  * Errors: bad code, or block != 0 with the cast code -> INVALID_ARG; other
- * block sizes -> UNSUPPORTED.
+ * block sizes, or a unit of more than 2^30 rows -> UNSUPPORTED.
  */
 hilore_status hilore_compress(const hilore_unit_desc *units, int n_units, int code, int block,
                               void *stream);
@@ -157,6 +157,7 @@ hilore_status hilore_compress(const hilore_unit_desc *units, int n_units, int co
  * back to bf16): xhat = bf16_RNE(value(code) * scale), elementwise; with
  * HILORE_CODE_FP8_E4M3FN_CAST xhat = value(code) exactly (NaN codes -> 0x7FC0).
  *   units[n_units]  host array; uses codes, scales (not with the cast code), xhat, rows, cols
+ * Errors as for hilore_compress.
  */
 hilore_status hilore_decompress(const hilore_unit_desc *units, int n_units, int code,
                                 int block, void *stream);

@@ -42,6 +42,7 @@ enum UnitUse : unsigned {
 hilore_status check_unit(const hilore_unit_desc &u, int block, unsigned use) {
   if (u.rows < 0 || u.cols < 0) return HILORE_ERR_INVALID_ARG;
   if (block > 0 && u.cols % block != 0) return HILORE_ERR_UNSUPPORTED;
+  if (u.rows > hilore::kRowsPerLaunch) return HILORE_ERR_UNSUPPORTED;
   if (u.rows == 0 || u.cols == 0) return HILORE_OK;
   if ((use & kUseX) != 0) {
     if (!u.x) return HILORE_ERR_INVALID_ARG;
@@ -71,7 +72,7 @@ hilore_status check_unit(const hilore_unit_desc &u, int block, unsigned use) {
 // Validate every unit, then launch in batches of kUnitsPerLaunch.
 template <typename Launch>
 hilore_status run_codec(const hilore_unit_desc *units, int n_units, int code, int block,
-                        unsigned use, bool stats, Launch launch) {
+                        unsigned use, bool stats, int lane_steps, Launch launch) {
   if (n_units < 0) return HILORE_ERR_INVALID_ARG;
   if (n_units == 0) return HILORE_OK;
   if (!units) return HILORE_ERR_INVALID_ARG;
@@ -82,35 +83,49 @@ hilore_status run_codec(const hilore_unit_desc *units, int n_units, int code, in
     const hilore_status st = check_unit(units[i], block, use);
     if (st != HILORE_OK) return st;
   }
-  for (int first = 0; first < n_units; first += hilore::kUnitsPerLaunch) {
-    CodecBatch b{};
-    int64_t rows = 0;
-    bool any_stats = false;
-    for (int i = first; i < n_units && b.n < hilore::kUnitsPerLaunch; ++i) {
-      const hilore_unit_desc &u = units[i];
-      if (u.rows == 0 || u.cols == 0) continue;
-      CodecUnit &c = b.u[b.n];
-      c.x = u.x;
-      c.codes = static_cast<uint8_t *>(u.codes);
-      c.scales = u.scales;
-      c.xhat = u.xhat;
-      c.ss_x = stats ? u.row_ss_x : nullptr;
-      c.ss_err = stats ? u.row_ss_err : nullptr;
-      c.rows = u.rows;
-      c.cols = u.cols;
-      c.ld = u.ld;
-      any_stats = any_stats || c.ss_x || c.ss_err;
-      b.row_begin[b.n] = rows;
-      rows += u.rows;
-      ++b.n;
-    }
-    if (b.n == 0) continue;
+  // consecutive units that share a row mapping go to one launch (at most
+  // kUnitsPerLaunch units and kRowsPerLaunch rows per launch)
+  CodecBatch b{};
+  int64_t rows = 0;
+  bool any_stats = false;
+  auto flush = [&]() -> hilore_status {
+    if (b.n == 0) return HILORE_OK;
     b.row_begin[b.n] = rows;
     b.stats = any_stats ? 1 : 0;
     const hilore_status st = hip_status(launch(b));
-    if (st != HILORE_OK) return st;
+    const int wl = b.wpr_log2;
+    b = CodecBatch{};
+    b.wpr_log2 = wl;
+    rows = 0;
+    any_stats = false;
+    return st;
+  };
+  for (int i = 0; i < n_units; ++i) {
+    const hilore_unit_desc &u = units[i];
+    if (u.rows == 0 || u.cols == 0) continue;
+    const int wl = hilore::codec_wpr_log2(u.cols, lane_steps);
+    if (b.n == hilore::kUnitsPerLaunch || (b.n > 0 && wl != b.wpr_log2) ||
+        rows + u.rows > hilore::kRowsPerLaunch) {
+      const hilore_status st = flush();
+      if (st != HILORE_OK) return st;
+    }
+    b.wpr_log2 = wl;
+    CodecUnit &c = b.u[b.n];
+    c.x = u.x;
+    c.codes = static_cast<uint8_t *>(u.codes);
+    c.scales = u.scales;
+    c.xhat = u.xhat;
+    c.ss_x = stats ? u.row_ss_x : nullptr;
+    c.ss_err = stats ? u.row_ss_err : nullptr;
+    c.rows = u.rows;
+    c.cols = u.cols;
+    c.ld = u.ld;
+    any_stats = any_stats || c.ss_x || c.ss_err;
+    b.row_begin[b.n] = rows;
+    rows += u.rows;
+    ++b.n;
   }
-  return HILORE_OK;
+  return flush();
 }
 
 }  // namespace
@@ -179,6 +194,7 @@ hilore_status hilore_compress(const hilore_unit_desc *units, int n_units, int co
                               void *stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   return run_codec(units, n_units, code, block, kUseX | kUseCodes | kUseScales | kUseStats, true,
+                   hilore::kCompressLaneSteps,
                    [&](const CodecBatch &b) { return hilore::launch_compress(b, code, block, s); });
 }
 
@@ -186,6 +202,7 @@ hilore_status hilore_decompress(const hilore_unit_desc *units, int n_units, int 
                                 int block, void *stream) {
   hipStream_t s = static_cast<hipStream_t>(stream);
   return run_codec(units, n_units, code, block, kUseCodes | kUseScales | kUseXhat, false,
+                   hilore::kDecompressLaneSteps,
                    [&](const CodecBatch &b) { return hilore::launch_decompress(b, code, block, s); });
 }
 

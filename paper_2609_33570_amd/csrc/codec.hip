@@ -7,15 +7,23 @@
 //   s = amax / Q, r = Q / amax (IEEE fp32 quotients), code = RNE(x * r),
 //   xhat = bf16_RNE(value(code) * s).
 //
-// Layout and mapping.  One wave owns one row at a time (rows of all units of
-// a launch are numbered consecutively and strided over the waves of the
-// grid).  Each lane moves 8 bf16 (one 128-bit load) per step, so a step of a
-// wave covers 512 consecutive columns and a block of BLOCK columns is held by
-// BLOCK/8 neighbouring lanes; its amax is a DPP/swizzle reduction inside that
-// lane group.  Codes leave as one 64-bit store per lane, scales as one 32-bit
-// store per block.  The optional per-row sums are kept per lane in a fixed
-// order and reduced once per row with a butterfly, so they do not depend on
-// the grid size.
+// Layout and mapping.  A row is swept by W = 2^wpr_log2 waves (1 to 16,
+// chosen from the row length by the host) and a launch is one pass over its
+// rows: a workgroup holds max(W, 4) waves and owns 4/W consecutive rows (W <
+// 4) or one row (W >= 4), then exits.  Each lane moves 8 bf16 (one 128-bit
+// load) per step, so a step of a wave covers 512 consecutive columns and a
+// block of BLOCK columns is held by BLOCK/8 neighbouring lanes; its amax is a
+// DPP/swizzle reduction inside that lane group.  Codes leave as one 64-bit
+// store per lane, scales as one 32-bit store per block.  Every access goes
+// through a buffer range bound to one row of its operand, so lanes past the
+// end of a row read zeros and drop their stores without branching, and the
+// row's base address stays in scalar registers.  Short-lived
+// workgroups that each cover a few KiB to a few tens of KiB of one row keep
+// the addresses in flight across the chip inside a narrow moving window,
+// which the HBM serves far better than thousands of waves each walking its
+// own row.  The optional per-row sums are kept per lane in a fixed order,
+// reduced per wave with a butterfly and across the row's waves in wave
+// order, so they depend only on the row length.
 //
 // The literal codec (code kCodeCast) is the paper's plain cast with no scale:
 // code = E4M3FN nearest-even of x where |x| <= 464 (448 for (448, 464]),
@@ -40,10 +48,10 @@
 namespace hilore {
 namespace {
 
-constexpr int kThreads = 256;
-constexpr int kWavesPerBlock = kThreads / kWave;
+constexpr int kMaxWaves = 16;  // waves per row at most (one workgroup)
+constexpr int kMaxThreads = kMaxWaves * kWave;
 constexpr int kColsPerStep = kWave * 8;
-constexpr int kUnroll = 4;
+constexpr int kUnroll = 4;  // loads a lane issues before using the first
 
 template <int CODE>
 struct QuotientTable {
@@ -68,15 +76,83 @@ __device__ __forceinline__ int find_unit(const CodecBatch &b, int64_t g) {
   return u;
 }
 
-// Scale s and reciprocal r of a block from its amax (see the file comment).
-// keep = 0 for a zero block (all codes forced to 0), else ~0.
+// The row (numbered over all units of the batch) and the position of this
+// wave among the W = 2^wl waves that sweep it (see the file comment).
+struct RowSlot {
+  int64_t g;  // may be >= the batch's row count for the last workgroup
+  int sub;    // 0 .. W-1
+};
+__device__ __forceinline__ RowSlot row_slot(int wl) {
+  const int wave = __builtin_amdgcn_readfirstlane((int)threadIdx.x / kWave);  // wave-uniform
+  const int rows_per_wg = wl >= 2 ? 1 : 4 >> wl;
+  return RowSlot{(int64_t)blockIdx.x * rows_per_wg + (wave >> wl), wave & ((1 << wl) - 1)};
+}
+
+// Sum of v over the W = 2^wl waves of each row of the workgroup, in wave
+// order, through red[] (one slot per wave); the result is valid in lane 0 of
+// the row's first wave.  Every thread of the workgroup must call it (it
+// holds a barrier when W > 1).
+__device__ __forceinline__ float row_sum(float v, int wl, float *red) {
+  v = wave_sum(v);
+  if (wl == 0) return v;
+  const int wave = threadIdx.x / kWave;
+  if ((threadIdx.x & (kWave - 1)) == 0) red[wave] = v;
+  __syncthreads();
+  if ((wave & ((1 << wl) - 1)) != 0) return v;
+  float t = red[wave];
+  for (int i = 1; i < (1 << wl); ++i) t += red[wave + i];
+  return t;
+}
+
+// Buffer range over one row of an operand (bytes [0, bytes) from base).
+// Loads past the range return 0 and stores past it are dropped.
+struct RowRsrc {
+  __amdgpu_buffer_rsrc_t r;
+};
+__device__ __forceinline__ RowRsrc row_rsrc(const void *base, uint32_t bytes) {
+  return RowRsrc{__builtin_amdgcn_make_buffer_rsrc(const_cast<void *>(base), 0, (int)bytes,
+                                                   0x00020000)};
+}
+constexpr uint32_t kOutOfRange = 0x80000000u;  // an offset past every row range
+constexpr int kStream = 2;  // cache policy: nontemporal (data is touched once)
+__device__ __forceinline__ u32x4 load_b128(const RowRsrc &r, uint32_t off) {
+  return __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(r.r, (int)off, 0,
+                                                                         kStream));
+}
+__device__ __forceinline__ u32x2 load_b64(const RowRsrc &r, uint32_t off) {
+  return __builtin_bit_cast(u32x2, __builtin_amdgcn_raw_buffer_load_b64(r.r, (int)off, 0,
+                                                                        kStream));
+}
+__device__ __forceinline__ uint32_t load_b32(const RowRsrc &r, uint32_t off) {
+  return __builtin_amdgcn_raw_buffer_load_b32(r.r, (int)off, 0, 0);
+}
+__device__ __forceinline__ void store_b128(const RowRsrc &r, uint32_t off, u32x4 v) {
+  __builtin_amdgcn_raw_buffer_store_b128(v, r.r, (int)off, 0,
+                                         kStream);
+}
+__device__ __forceinline__ void store_b64(const RowRsrc &r, uint32_t off, u32x2 v) {
+  __builtin_amdgcn_raw_buffer_store_b64(v, r.r, (int)off, 0,
+                                        kStream);
+}
+__device__ __forceinline__ void store_b32(const RowRsrc &r, uint32_t off, uint32_t v) {
+  __builtin_amdgcn_raw_buffer_store_b32(v, r.r, (int)off, 0, kStream);
+}
+
+// acc + lo*lo + hi*hi over the two bf16 halves of w (v_dot2c_f32_bf16).
+__device__ __forceinline__ float dot2_bf16(uint32_t w, float acc) {
+  const bf16x2 v = __builtin_bit_cast(bf16x2, w);
+  return __builtin_amdgcn_fdot2_f32_bf16(v, v, acc, false);
+}
+
+// Scale s and reciprocal r of a block from its amax, given as bf16 bits
+// (see the file comment).  keep = 0 for a zero block (all codes forced to
+// 0), else ~0.
 template <int CODE>
-__device__ __forceinline__ void block_quotients(float amax, const uint32_t *tab_s,
+__device__ __forceinline__ void block_quotients(uint32_t amax_bits, const uint32_t *tab_s,
                                                 const uint32_t *tab_r, float &s, float &r,
                                                 uint32_t &keep) {
-  const uint32_t ab = __float_as_uint(amax);
-  const uint32_t k = (ab >> 16) & 0x7Fu;
-  const int e = (int)(ab >> 23) - 127;
+  const uint32_t k = amax_bits & 0x7Fu;
+  const int e = (int)(amax_bits >> 7) - 127;
   const bool zero = e < -64;  // amax < 2^-64
   const uint32_t sb = tab_s[k] + ((uint32_t)e << 23);
   const uint32_t rb = tab_r[k] - ((uint32_t)e << 23);
@@ -108,9 +184,11 @@ __device__ __forceinline__ u32x2 encode8(const float v[8], uint32_t keep, float 
   } else {
     // v_cvt_pk_fp8_f32: round to nearest even onto OCP E4M3FN, sign kept
     // (checked bit for bit against the software rule for every |v| <= 448).
-    int lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], 0, false);
+    // the first conversion of each word writes its low half; the high half
+    // it keeps (here: whatever keep holds) is overwritten by the second
+    int lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[0], v[1], (int)keep, false);
     lo = __builtin_amdgcn_cvt_pk_fp8_f32(v[2], v[3], lo, true);
-    int hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[4], v[5], 0, false);
+    int hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[4], v[5], (int)keep, false);
     hi = __builtin_amdgcn_cvt_pk_fp8_f32(v[6], v[7], hi, true);
     out.x = (uint32_t)lo & keep;
     out.y = (uint32_t)hi & keep;
@@ -180,38 +258,42 @@ __device__ __forceinline__ uint32_t uncast2(uint32_t w) {
   return lo | (hi << 16);
 }
 
-// The literal cast, same row-per-wave mapping as compress_kernel.
+// The literal cast, same mapping as compress_kernel.
 template <bool STATS>
-__global__ __launch_bounds__(kThreads) void cast_kernel(const CodecBatch b) {
+__global__ __launch_bounds__(kMaxThreads) void cast_kernel(const CodecBatch b) {
+  __shared__ float red_x[kMaxWaves], red_e[kMaxWaves];
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t n_waves = (int64_t)gridDim.x * kWavesPerBlock;
-  const int64_t total = b.row_begin[b.n];
-  for (int64_t g = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; g < total;
-       g += n_waves) {
-    const int u = find_unit(b, g);
-    const CodecUnit &d = b.u[u];
-    const int64_t row = g - b.row_begin[u];
-    const int64_t cols = d.cols;
-    const u32x4 *xr = reinterpret_cast<const u32x4 *>(d.x + row * d.ld);
-    u32x2 *cr = reinterpret_cast<u32x2 *>(d.codes + row * cols);
-    float acc_x = 0.0f, acc_e = 0.0f;
-    for (int64_t c0 = 0; c0 < cols; c0 += kColsPerStep * kUnroll) {
+  const int wl = b.wpr_log2;
+  const RowSlot rs = row_slot(wl);
+  float acc_x = 0.0f, acc_e = 0.0f;
+  float *out_x = nullptr, *out_e = nullptr;  // this row's sums (lane 0 of wave 0)
+  if (rs.g < b.row_begin[b.n]) {
+    const int u = find_unit(b, rs.g);
+    const CodecUnit *dp = &b.u[u];
+    const int64_t row = rs.g - b.row_begin[u];
+    if (rs.sub == 0 && lane == 0) {
+      out_x = dp->ss_x ? dp->ss_x + row : nullptr;
+      out_e = dp->ss_err ? dp->ss_err + row : nullptr;
+    }
+    const uint32_t cols = (uint32_t)dp->cols;
+    const RowRsrc rx = row_rsrc(dp->x + row * dp->ld, cols * 2);
+    const RowRsrc rc = row_rsrc(dp->codes + row * (int64_t)cols, cols);
+    const uint32_t step = (uint32_t)kColsPerStep << wl;
+    // lanes past the end of the row cast zeros (adding 0 to the sums) and
+    // their stores are dropped
+    for (uint32_t c0 = (uint32_t)rs.sub * kColsPerStep; c0 < cols; c0 += kUnroll * step) {
       u32x4 w[kUnroll];
 #pragma unroll
-      for (int i = 0; i < kUnroll; ++i) {
-        const int64_t col = c0 + i * kColsPerStep + lane * 8;
-        w[i] = col < cols ? __builtin_nontemporal_load(xr + col / 8) : u32x4{0, 0, 0, 0};
-      }
+      for (int i = 0; i < kUnroll; ++i) w[i] = load_b128(rx, (c0 + i * step + lane * 8) * 2);
 #pragma unroll
       for (int i = 0; i < kUnroll; ++i) {
-        const int64_t col = c0 + i * kColsPerStep + lane * 8;
-        if (col >= cols) continue;
+        if (c0 + i * step >= cols) break;  // wave-uniform
         float x[8], q[8];
         x[0] = bf16_lo(w[i].x); x[1] = bf16_hi(w[i].x);
         x[2] = bf16_lo(w[i].y); x[3] = bf16_hi(w[i].y);
         x[4] = bf16_lo(w[i].z); x[5] = bf16_hi(w[i].z);
         x[6] = bf16_lo(w[i].w); x[7] = bf16_hi(w[i].w);
-        __builtin_nontemporal_store(cast8(x, q), cr + col / 8);
+        store_b64(rc, c0 + i * step + lane * 8, cast8(x, q));
         if constexpr (STATS) {
 #pragma unroll
           for (int j = 0; j < 8; ++j) {
@@ -222,53 +304,46 @@ __global__ __launch_bounds__(kThreads) void cast_kernel(const CodecBatch b) {
         }
       }
     }
-    if constexpr (STATS) {
-      acc_x = wave_sum(acc_x);
-      acc_e = wave_sum(acc_e);
-      if (lane == 0) {
-        if (d.ss_x) d.ss_x[row] = acc_x;
-        if (d.ss_err) d.ss_err[row] = acc_e;
-      }
-    }
+  }
+  if constexpr (STATS) {
+    acc_x = row_sum(acc_x, wl, red_x);
+    acc_e = row_sum(acc_e, wl, red_e);
+    if (out_x) *out_x = acc_x;
+    if (out_e) *out_e = acc_e;
   }
 }
 
-__global__ __launch_bounds__(kThreads) void uncast_kernel(const CodecBatch b) {
+__global__ __launch_bounds__(kMaxThreads) void uncast_kernel(const CodecBatch b) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t n_waves = (int64_t)gridDim.x * kWavesPerBlock;
-  const int64_t total = b.row_begin[b.n];
-  for (int64_t g = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; g < total;
-       g += n_waves) {
-    const int u = find_unit(b, g);
-    const CodecUnit &d = b.u[u];
-    const int64_t row = g - b.row_begin[u];
-    const int64_t cols = d.cols;
-    const u32x2 *cr = reinterpret_cast<const u32x2 *>(d.codes + row * cols);
-    u32x4 *hr = reinterpret_cast<u32x4 *>(d.xhat + row * cols);
-    for (int64_t c0 = 0; c0 < cols; c0 += kColsPerStep * kUnroll) {
-      u32x2 c[kUnroll];
+  const int wl = b.wpr_log2;
+  const RowSlot rs = row_slot(wl);
+  if (rs.g >= b.row_begin[b.n]) return;
+  const int u = find_unit(b, rs.g);
+  const CodecUnit &d = b.u[u];
+  const int64_t row = rs.g - b.row_begin[u];
+  const uint32_t cols = (uint32_t)d.cols;
+  const RowRsrc rc = row_rsrc(d.codes + row * (int64_t)cols, cols);
+  const RowRsrc rh = row_rsrc(d.xhat + row * (int64_t)cols, cols * 2);
+  const uint32_t step = (uint32_t)kColsPerStep << wl;
+  for (uint32_t c0 = (uint32_t)rs.sub * kColsPerStep; c0 < cols; c0 += kUnroll * step) {
+    u32x2 c[kUnroll];
 #pragma unroll
-      for (int i = 0; i < kUnroll; ++i) {
-        const int64_t col = c0 + i * kColsPerStep + lane * 8;
-        c[i] = col < cols ? __builtin_nontemporal_load(cr + col / 8) : u32x2{0, 0};
-      }
+    for (int i = 0; i < kUnroll; ++i) c[i] = load_b64(rc, c0 + i * step + lane * 8);
 #pragma unroll
-      for (int i = 0; i < kUnroll; ++i) {
-        const int64_t col = c0 + i * kColsPerStep + lane * 8;
-        if (col < cols) {
-          const u32x4 h = {uncast2<false>(c[i].x), uncast2<true>(c[i].x),
-                           uncast2<false>(c[i].y), uncast2<true>(c[i].y)};
-          __builtin_nontemporal_store(h, hr + col / 8);
-        }
-      }
+    for (int i = 0; i < kUnroll; ++i) {
+      if (c0 + i * step >= cols) break;  // wave-uniform
+      const u32x4 h = {uncast2<false>(c[i].x), uncast2<true>(c[i].x), uncast2<false>(c[i].y),
+                       uncast2<true>(c[i].y)};
+      store_b128(rh, (c0 + i * step + lane * 8) * 2, h);
     }
   }
 }
 
 template <int CODE, int BLOCK, bool STATS>
-__global__ __launch_bounds__(kThreads) void compress_kernel(const CodecBatch b) {
+__global__ __launch_bounds__(kMaxThreads) void compress_kernel(const CodecBatch b) {
   constexpr int kLanesPerBlock = BLOCK / 8;
   __shared__ uint32_t tab_s[128], tab_r[128];
+  __shared__ float red_x[kMaxWaves], red_e[kMaxWaves];
   if (threadIdx.x < 128) {
     tab_s[threadIdx.x] = kQuot<CODE>.s[threadIdx.x];
     tab_r[threadIdx.x] = kQuot<CODE>.r[threadIdx.x];
@@ -276,38 +351,44 @@ __global__ __launch_bounds__(kThreads) void compress_kernel(const CodecBatch b) 
   __syncthreads();
 
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t n_waves = (int64_t)gridDim.x * kWavesPerBlock;
-  const int64_t total = b.row_begin[b.n];
-  for (int64_t g = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; g < total;
-       g += n_waves) {
-    const int u = find_unit(b, g);
-    const CodecUnit &d = b.u[u];
-    const int64_t row = g - b.row_begin[u];
-    const int64_t cols = d.cols;
-    const u32x4 *xr = reinterpret_cast<const u32x4 *>(d.x + row * d.ld);
-    u32x2 *cr = reinterpret_cast<u32x2 *>(d.codes + row * cols);
-    float *sr = d.scales + row * (cols / BLOCK);
-    float acc_x = 0.0f, acc_e = 0.0f;
-
-    for (int64_t c0 = 0; c0 < cols; c0 += kColsPerStep * kUnroll) {
+  const int wl = b.wpr_log2;
+  const RowSlot rs = row_slot(wl);
+  float acc_x = 0.0f, acc_e = 0.0f;
+  float *out_x = nullptr, *out_e = nullptr;  // this row's sums (lane 0 of wave 0)
+  if (rs.g < b.row_begin[b.n]) {
+    const int u = find_unit(b, rs.g);
+    const CodecUnit *dp = &b.u[u];
+    const int64_t row = rs.g - b.row_begin[u];
+    if (rs.sub == 0 && lane == 0) {
+      out_x = dp->ss_x ? dp->ss_x + row : nullptr;
+      out_e = dp->ss_err ? dp->ss_err + row : nullptr;
+    }
+    // One buffer range per operand row: lanes past the end of the row load
+    // zeros (a zero block: scale 0) and their stores fall outside the range
+    // and are dropped, so the loop needs no per-lane branches.
+    const uint32_t cols = (uint32_t)dp->cols;
+    const RowRsrc rx = row_rsrc(dp->x + row * dp->ld, cols * 2);
+    const RowRsrc rc = row_rsrc(dp->codes + row * (int64_t)cols, cols);
+    const RowRsrc rsc = row_rsrc(dp->scales + row * (int64_t)(cols / BLOCK), cols / BLOCK * 4);
+    const bool leader = (lane & (kLanesPerBlock - 1)) == 0;
+    const uint32_t step = (uint32_t)kColsPerStep << wl;
+    // All of a lane's loads of a round (up to kUnroll steps of the row) are
+    // issued before any of them is used; trip counts are wave-uniform.
+    for (uint32_t c0 = (uint32_t)rs.sub * kColsPerStep; c0 < cols; c0 += kUnroll * step) {
       u32x4 w[kUnroll];
 #pragma unroll
-      for (int i = 0; i < kUnroll; ++i) {
-        const int64_t col = c0 + i * kColsPerStep + lane * 8;
-        w[i] = col < cols ? __builtin_nontemporal_load(xr + col / 8) : u32x4{0, 0, 0, 0};
-      }
+      for (int i = 0; i < kUnroll; ++i)
+        w[i] = load_b128(rx, (c0 + i * step + lane * 8) * 2);
 #pragma unroll
       for (int i = 0; i < kUnroll; ++i) {
-        const int64_t col = c0 + i * kColsPerStep + lane * 8;
-        if (c0 + i * kColsPerStep >= cols) break;  // wave-uniform
+        if (c0 + i * step >= cols) break;  // wave-uniform
+        const uint32_t col = c0 + i * step + lane * 8;
         float x[8];
         x[0] = bf16_lo(w[i].x); x[1] = bf16_hi(w[i].x);
         x[2] = bf16_lo(w[i].y); x[3] = bf16_hi(w[i].y);
         x[4] = bf16_lo(w[i].z); x[5] = bf16_hi(w[i].z);
         x[6] = bf16_lo(w[i].w); x[7] = bf16_hi(w[i].w);
-        float am = fmaxf(fmaxf(fmaxf(fabsf(x[0]), fabsf(x[1])), fmaxf(fabsf(x[2]), fabsf(x[3]))),
-                         fmaxf(fmaxf(fabsf(x[4]), fabsf(x[5])), fmaxf(fabsf(x[6]), fabsf(x[7]))));
-        am = group_max<kLanesPerBlock>(am);
+        const uint32_t am = group_max_u32<kLanesPerBlock>(absmax_bf16x8(w[i]));
         float s, r;
         uint32_t keep;
         block_quotients<CODE>(am, tab_s, tab_r, s, r, keep);
@@ -315,11 +396,14 @@ __global__ __launch_bounds__(kThreads) void compress_kernel(const CodecBatch b) 
 #pragma unroll
         for (int j = 0; j < 8; ++j) v[j] = x[j] * r;
         const u32x2 code = encode8<CODE>(v, keep, q);
-        if (col < cols) {
-          __builtin_nontemporal_store(code, cr + col / 8);
-          if ((lane & (kLanesPerBlock - 1)) == 0) sr[col / BLOCK] = s;
-        }
+        store_b64(rc, col, code);
+        store_b32(rsc, leader ? col / BLOCK * 4 : kOutOfRange, __float_as_uint(s));
         if constexpr (STATS) {
+          // sum x^2 straight from the packed bf16 pairs (products are exact)
+          acc_x = dot2_bf16(w[i].x, acc_x);
+          acc_x = dot2_bf16(w[i].y, acc_x);
+          acc_x = dot2_bf16(w[i].z, acc_x);
+          acc_x = dot2_bf16(w[i].w, acc_x);
 #pragma unroll
           for (int j = 0; j < 8; j += 2) {
             const uint32_t h = pack_bf16(q[j] * s, q[j + 1] * s);
@@ -327,88 +411,84 @@ __global__ __launch_bounds__(kThreads) void compress_kernel(const CodecBatch b) 
             const float e1 = bf16_hi(h) - x[j + 1];
             acc_e = fmaf(e0, e0, acc_e);
             acc_e = fmaf(e1, e1, acc_e);
-            acc_x = fmaf(x[j], x[j], acc_x);
-            acc_x = fmaf(x[j + 1], x[j + 1], acc_x);
           }
         }
       }
     }
-    if constexpr (STATS) {
-      acc_x = wave_sum(acc_x);
-      acc_e = wave_sum(acc_e);
-      if (lane == 0) {
-        if (d.ss_x) d.ss_x[row] = acc_x;
-        if (d.ss_err) d.ss_err[row] = acc_e;
-      }
-    }
+  }
+  if constexpr (STATS) {
+    acc_x = row_sum(acc_x, wl, red_x);
+    acc_e = row_sum(acc_e, wl, red_e);
+    if (out_x) *out_x = acc_x;
+    if (out_e) *out_e = acc_e;
   }
 }
 
 template <int CODE, int BLOCK>
-__global__ __launch_bounds__(kThreads) void decompress_kernel(const CodecBatch b) {
+__global__ __launch_bounds__(kMaxThreads) void decompress_kernel(const CodecBatch b) {
   const int lane = threadIdx.x & (kWave - 1);
-  const int64_t n_waves = (int64_t)gridDim.x * kWavesPerBlock;
-  const int64_t total = b.row_begin[b.n];
-  for (int64_t g = (int64_t)blockIdx.x * kWavesPerBlock + threadIdx.x / kWave; g < total;
-       g += n_waves) {
-    const int u = find_unit(b, g);
-    const CodecUnit &d = b.u[u];
-    const int64_t row = g - b.row_begin[u];
-    const int64_t cols = d.cols;
-    const u32x2 *cr = reinterpret_cast<const u32x2 *>(d.codes + row * cols);
-    const float *sr = d.scales + row * (cols / BLOCK);
-    u32x4 *hr = reinterpret_cast<u32x4 *>(d.xhat + row * cols);
-    for (int64_t c0 = 0; c0 < cols; c0 += kColsPerStep * kUnroll) {
-      u32x2 c[kUnroll];
-      float s[kUnroll];
+  const int wl = b.wpr_log2;
+  const RowSlot rs = row_slot(wl);
+  if (rs.g >= b.row_begin[b.n]) return;
+  const int u = find_unit(b, rs.g);
+  const CodecUnit &d = b.u[u];
+  const int64_t row = rs.g - b.row_begin[u];
+  const uint32_t cols = (uint32_t)d.cols;
+  const RowRsrc rc = row_rsrc(d.codes + row * (int64_t)cols, cols);
+  const RowRsrc rsc = row_rsrc(d.scales + row * (int64_t)(cols / BLOCK), cols / BLOCK * 4);
+  const RowRsrc rh = row_rsrc(d.xhat + row * (int64_t)cols, cols * 2);
+  const uint32_t step = (uint32_t)kColsPerStep << wl;
+  // lanes past the end of the row read zeros and their stores are dropped
+  for (uint32_t c0 = (uint32_t)rs.sub * kColsPerStep; c0 < cols; c0 += kUnroll * step) {
+    u32x2 c[kUnroll];
+    float s[kUnroll];
 #pragma unroll
-      for (int i = 0; i < kUnroll; ++i) {
-        const int64_t col = c0 + i * kColsPerStep + lane * 8;
-        const bool in = col < cols;
-        c[i] = in ? __builtin_nontemporal_load(cr + col / 8) : u32x2{0, 0};
-        s[i] = in ? sr[col / BLOCK] : 0.0f;
-      }
+    for (int i = 0; i < kUnroll; ++i) {
+      const uint32_t col = c0 + i * step + lane * 8;
+      c[i] = load_b64(rc, col);
+      s[i] = __uint_as_float(load_b32(rsc, col / BLOCK * 4));
+    }
 #pragma unroll
-      for (int i = 0; i < kUnroll; ++i) {
-        const int64_t col = c0 + i * kColsPerStep + lane * 8;
-        if (col < cols) {
-          float q[8];
-          decode8<CODE>(c[i], q);
-          u32x4 h;
-          h.x = pack_bf16(q[0] * s[i], q[1] * s[i]);
-          h.y = pack_bf16(q[2] * s[i], q[3] * s[i]);
-          h.z = pack_bf16(q[4] * s[i], q[5] * s[i]);
-          h.w = pack_bf16(q[6] * s[i], q[7] * s[i]);
-          __builtin_nontemporal_store(h, hr + col / 8);
-        }
-      }
+    for (int i = 0; i < kUnroll; ++i) {
+      if (c0 + i * step >= cols) break;  // wave-uniform
+      float q[8];
+      decode8<CODE>(c[i], q);
+      u32x4 h;
+      h.x = pack_bf16(q[0] * s[i], q[1] * s[i]);
+      h.y = pack_bf16(q[2] * s[i], q[3] * s[i]);
+      h.z = pack_bf16(q[4] * s[i], q[5] * s[i]);
+      h.w = pack_bf16(q[6] * s[i], q[7] * s[i]);
+      store_b128(rh, (c0 + i * step + lane * 8) * 2, h);
     }
   }
 }
 
-int grid_for(int64_t rows) {
-  // Enough 4-wave workgroups to keep every CU of the chip busy (256 CUs,
-  // several resident workgroups each); fewer when there are fewer rows.
-  const int64_t want = (rows + kWavesPerBlock - 1) / kWavesPerBlock;
-  const int64_t cap = 256 * 8;
-  return (int)(want < cap ? (want > 0 ? want : 1) : cap);
+// One workgroup per row (W >= 4) or per 4/W rows, one pass over the batch.
+struct Launch {
+  dim3 grid, block;
+};
+Launch launch_shape(const CodecBatch &b) {
+  const int wl = b.wpr_log2;
+  const int64_t rows_per_wg = wl >= 2 ? 1 : 4 >> wl;
+  const int64_t total = b.row_begin[b.n];
+  const int64_t grid = (total + rows_per_wg - 1) / rows_per_wg;
+  return Launch{dim3((unsigned)(grid > 0 ? grid : 1)), dim3(kWave << (wl >= 2 ? wl : 2))};
 }
 
 template <int CODE, int BLOCK>
 hipError_t compress_dispatch(const CodecBatch &b, hipStream_t s) {
-  const int grid = grid_for(b.row_begin[b.n]);
+  const Launch l = launch_shape(b);
   if (b.stats)
-    hipLaunchKernelGGL((compress_kernel<CODE, BLOCK, true>), dim3(grid), dim3(kThreads), 0, s, b);
+    hipLaunchKernelGGL((compress_kernel<CODE, BLOCK, true>), l.grid, l.block, 0, s, b);
   else
-    hipLaunchKernelGGL((compress_kernel<CODE, BLOCK, false>), dim3(grid), dim3(kThreads), 0, s,
-                       b);
+    hipLaunchKernelGGL((compress_kernel<CODE, BLOCK, false>), l.grid, l.block, 0, s, b);
   return hipGetLastError();
 }
 
 template <int CODE, int BLOCK>
 hipError_t decompress_dispatch(const CodecBatch &b, hipStream_t s) {
-  const int grid = grid_for(b.row_begin[b.n]);
-  hipLaunchKernelGGL((decompress_kernel<CODE, BLOCK>), dim3(grid), dim3(kThreads), 0, s, b);
+  const Launch l = launch_shape(b);
+  hipLaunchKernelGGL((decompress_kernel<CODE, BLOCK>), l.grid, l.block, 0, s, b);
   return hipGetLastError();
 }
 
@@ -436,11 +516,11 @@ hipError_t decompress_code(const CodecBatch &b, int block, hipStream_t s) {
 
 hipError_t launch_compress(const CodecBatch &b, int code, int block, hipStream_t s) {
   if (code == kCodeCast) {
-    const int grid = grid_for(b.row_begin[b.n]);
+    const Launch l = launch_shape(b);
     if (b.stats)
-      hipLaunchKernelGGL((cast_kernel<true>), dim3(grid), dim3(kThreads), 0, s, b);
+      hipLaunchKernelGGL((cast_kernel<true>), l.grid, l.block, 0, s, b);
     else
-      hipLaunchKernelGGL((cast_kernel<false>), dim3(grid), dim3(kThreads), 0, s, b);
+      hipLaunchKernelGGL((cast_kernel<false>), l.grid, l.block, 0, s, b);
     return hipGetLastError();
   }
   return code == kCodeInt8 ? compress_code<kCodeInt8>(b, block, s)
@@ -449,7 +529,8 @@ hipError_t launch_compress(const CodecBatch &b, int code, int block, hipStream_t
 
 hipError_t launch_decompress(const CodecBatch &b, int code, int block, hipStream_t s) {
   if (code == kCodeCast) {
-    hipLaunchKernelGGL(uncast_kernel, dim3(grid_for(b.row_begin[b.n])), dim3(kThreads), 0, s, b);
+    const Launch l = launch_shape(b);
+    hipLaunchKernelGGL(uncast_kernel, l.grid, l.block, 0, s, b);
     return hipGetLastError();
   }
   return code == kCodeInt8 ? decompress_code<kCodeInt8>(b, block, s)

@@ -32,25 +32,41 @@ enum : int {
   kDppRowMirror = 0x140,
 };
 
+// v and its DPP neighbour combined by an unsigned max: the DPP move folds
+// into v_max_u32_dpp (lanes without a source read 0, the identity).
 template <int CTRL>
-__device__ __forceinline__ float dpp_f32(float v) {
-  return __int_as_float(__builtin_amdgcn_update_dpp(0, __float_as_int(v), CTRL, 0xF, 0xF, false));
+__device__ __forceinline__ uint32_t dpp_max_u32(uint32_t v) {
+  return max(v, (uint32_t)__builtin_amdgcn_mov_dpp((int)v, CTRL, 0xF, 0xF, true));
 }
 
-// Max over aligned groups of L lanes (L = 4, 8, 16 or 32); every lane of the
-// group receives the group maximum.  After the quad steps each quad holds its
-// max; the half-row mirror pairs quads 0<->1 and 2<->3, the row mirror pairs
-// the two halves of a 16-lane row, and a swizzle pairs the two rows of 32.
+// Unsigned max over aligned groups of L lanes (L = 4, 8, 16 or 32); every
+// lane of the group receives the group maximum.  After the quad steps each
+// quad holds its max; the half-row mirror pairs quads 0<->1 and 2<->3, the
+// row mirror pairs the two halves of a 16-lane row, and a swizzle pairs the
+// two rows of 32.
 template <int L>
-__device__ __forceinline__ float group_max(float v) {
+__device__ __forceinline__ uint32_t group_max_u32(uint32_t v) {
   static_assert(L == 4 || L == 8 || L == 16 || L == 32, "group size");
-  v = fmaxf(v, dpp_f32<kDppQuadXor1>(v));
-  v = fmaxf(v, dpp_f32<kDppQuadXor2>(v));
-  if constexpr (L >= 8) v = fmaxf(v, dpp_f32<kDppRowHalfMirror>(v));
-  if constexpr (L >= 16) v = fmaxf(v, dpp_f32<kDppRowMirror>(v));
-  if constexpr (L >= 32)
-    v = fmaxf(v, __int_as_float(__builtin_amdgcn_ds_swizzle(__float_as_int(v), 0x401F)));
+  v = dpp_max_u32<kDppQuadXor1>(v);
+  v = dpp_max_u32<kDppQuadXor2>(v);
+  if constexpr (L >= 8) v = dpp_max_u32<kDppRowHalfMirror>(v);
+  if constexpr (L >= 16) v = dpp_max_u32<kDppRowMirror>(v);
+  if constexpr (L >= 32) v = max(v, (uint32_t)__builtin_amdgcn_ds_swizzle((int)v, 0x401F));
   return v;
+}
+
+// Largest magnitude of the 8 bf16 values of w, as bf16 bits in the low half
+// (non-negative bf16 patterns order like their values; NaN is out of
+// contract).
+__device__ __forceinline__ uint32_t absmax_bf16x8(u32x4 w) {
+  typedef unsigned short u16x2 __attribute__((ext_vector_type(2)));
+  const u16x2 a = __builtin_bit_cast(u16x2, w.x & 0x7FFF7FFFu);
+  const u16x2 b = __builtin_bit_cast(u16x2, w.y & 0x7FFF7FFFu);
+  const u16x2 c = __builtin_bit_cast(u16x2, w.z & 0x7FFF7FFFu);
+  const u16x2 d = __builtin_bit_cast(u16x2, w.w & 0x7FFF7FFFu);
+  const u16x2 m = __builtin_elementwise_max(__builtin_elementwise_max(a, b),
+                                            __builtin_elementwise_max(c, d));
+  return max((uint32_t)m.x, (uint32_t)m.y);
 }
 
 // Sum over the whole wave as a butterfly (xor 1, 2, 4, ..., 32).  Addition

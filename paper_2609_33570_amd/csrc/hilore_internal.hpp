@@ -26,13 +26,30 @@ struct CodecUnit {
 
 // Units encoded/decoded by one launch travel by value in the kernel
 // arguments, so a call needs no device workspace and no host->device copy.
+// The units of one launch share the number of waves that sweep a row.
 constexpr int kUnitsPerLaunch = 16;
+constexpr int64_t kRowsPerLaunch = int64_t(1) << 30;  // bound on a launch's grid
 struct CodecBatch {
   CodecUnit u[kUnitsPerLaunch];
   int64_t row_begin[kUnitsPerLaunch + 1];  // prefix sum of rows over u[]
   int n;
-  int stats;  // compress: write row sums
+  int stats;     // compress: write row sums
+  int wpr_log2;  // log2 of the waves per row, 0..4
 };
+
+// Waves per row (as log2, 0..4) for rows of `cols` columns: the fewest that
+// leave each lane at most `lane_steps` steps of 8 columns (measured on
+// MI355X over rows of 3584 to 18944 columns: about 5 steps per lane suits
+// both directions; fewer waves per row leave the HBM less evenly loaded,
+// more waves per row add per-workgroup overhead).
+constexpr int kCompressLaneSteps = 5;
+constexpr int kDecompressLaneSteps = 5;
+inline int codec_wpr_log2(int64_t cols, int lane_steps) {
+  const int64_t steps = (cols + 7) / 8;
+  int wl = 0;
+  while (wl < 4 && (int64_t(64 * lane_steps) << wl) < steps) ++wl;
+  return wl;
+}
 
 hipError_t launch_compress(const CodecBatch &b, int code, int block, hipStream_t s);
 hipError_t launch_decompress(const CodecBatch &b, int code, int block, hipStream_t s);
