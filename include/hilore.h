@@ -8,6 +8,7 @@
  *   after forward   encode the L candidates                 -> hilore_compress
  *   Coefficients    per-token GRPO loss coefficients omega  -> hilore_grpo_coeffs
  *   Exposure, psi   per-unit exposure and risk              -> hilore_unit_exposure_risk
+ *   Allocate        joint H/L/R choice under memory and risk -> hilore_allocate
  *   in backward     reconstruct L units                     -> hilore_decompress
  *                   and consume them in the weight gradient -> hilore_dequant_wgrad
  *
@@ -24,7 +25,8 @@
  *     device state, so argument errors are reported even without a GPU.
  *   - bf16 tensors are passed as uint16_t* (raw bit patterns).
  *   - Alignment: every tensor pointer must be 16-byte aligned, except the
- *     per-unit outputs of hilore_unit_exposure_risk (4-byte aligned).
+ *     per-unit outputs of hilore_unit_exposure_risk (4-byte aligned) and the
+ *     per-unit arrays of hilore_allocate (8-byte aligned for fp64).
  *   - The functions are re-entrant; calls on different streams may run
  *     concurrently.  No C++ exception crosses this interface.
  *   - Results do not depend on the launch configuration: every reduction is
@@ -45,6 +47,7 @@ typedef enum hilore_status {
   HILORE_ERR_INVALID_ARG = 1, /* null pointer, negative size, bad enum value      */
   HILORE_ERR_ALIGNMENT = 2,   /* pointer not 16-byte aligned, or bad row stride    */
   HILORE_ERR_UNSUPPORTED = 3, /* valid but unsupported shape (e.g. G > 64)         */
+  HILORE_ERR_WORKSPACE = 4,   /* caller-supplied workspace smaller than required   */
   HILORE_ERR_HIP = 5          /* a HIP launch failed (hipGetLastError)             */
 } hilore_status;
 
@@ -200,6 +203,50 @@ hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask,
 hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, int code,
                                    int block, const uint16_t *dy, float *dw, int64_t K,
                                    int64_t M, int64_t N, int accumulate, void *stream);
+
+/*
+ * Joint H/L/R recovery allocation of one microbatch (Sec. 3.4 Eq.
+ * joint-allocation, solved exactly on the conservative grid of App. B.2:
+ * Eqs. allocation-grid, allocation-integer-costs, allocation-dp, the tie rules
+ * and boundary cases that follow them; available actions of App. B.3 Eq.
+ * available-recovery-actions).  Actions: 0 = R (recompute; zero utility,
+ * memory and risk), 1 = H (keep; tau_h, dm_h, risk 0), 2 = L (low precision;
+ * tau_l, dm_l, risk psi).
+ *   q[u]         u8: retained representation of unit u under the plan (0/1/2):
+ *                H allows {H, L, R}, L allows {L, R}, anything else only R
+ *   verified[u]  u8: bit a set when action a is verified for unit u
+ *   tau_h, tau_l, dm_h, dm_l, psi   f64 [n_units]: utilities (Delta tau), memory
+ *                costs (Delta m) and the L risk (psi_u, e.g. from
+ *                hilore_unit_exposure_risk's exposure times the calibration
+ *                factor kappa * ebar of App. B.1 Eq. app-risk-score)
+ *   m_res        residual memory budget B - M_peak (>= 0), delta_b risk budget (>= 0)
+ *   n_b, n_d     grid intervals N_B, N_delta (1024 in the paper), 1 .. 4096
+ * A non-R action is available only if verified, allowed by q, with utility
+ * > 0 and finite non-negative costs; L also needs delta_b > 0.  Costs round up
+ * to integer grid steps (ceil(cost / (budget / n))); a zero budget keeps one
+ * state on its axis and admits only zero costs.  Within a state, actions are
+ * tried in the order R, H, L and replace the incumbent only when strictly
+ * better; the terminal state is the best value, ties to lower risk cost, then
+ * lower memory cost; actions come from backtracking.
+ * Outputs (device): action u8 [n_units]; totals f64 [3] = (summed utility,
+ * memory, risk of the chosen actions, the latter two summed in unit order);
+ * jk i64 [2] = terminal integer memory and risk costs.  All arithmetic is
+ * fp64 in the order of a sequential implementation, so results are exact.
+ * workspace: device memory of at least hilore_allocate_workspace_bytes(n_units,
+ * n_b, n_d) bytes, 16-byte aligned, owned by the caller (about 8.9 MB per
+ * table plus 279 KB per unit for a 1025 x 1025 grid); its contents on entry
+ * do not matter.  Calls that share a workspace must not overlap.
+ * Errors: negative or non-finite budgets, n_b or n_d < 1, null pointers ->
+ * INVALID_ARG; n_b or n_d > 4096, n_units > 2^20 -> UNSUPPORTED; workspace too
+ * small -> WORKSPACE.
+ */
+size_t hilore_allocate_workspace_bytes(int n_units, int n_b, int n_d);
+hilore_status hilore_allocate(int n_units, const uint8_t *q, const uint8_t *verified,
+                              const double *tau_h, const double *tau_l, const double *dm_h,
+                              const double *dm_l, const double *psi, double m_res,
+                              double delta_b, int n_b, int n_d, uint8_t *action, double *totals,
+                              int64_t *jk, void *workspace, size_t workspace_bytes,
+                              void *stream);
 
 #ifdef __cplusplus
 }

@@ -138,6 +138,7 @@ const char *hilore_status_string(int status) {
     case HILORE_ERR_INVALID_ARG: return "HILORE_ERR_INVALID_ARG";
     case HILORE_ERR_ALIGNMENT: return "HILORE_ERR_ALIGNMENT";
     case HILORE_ERR_UNSUPPORTED: return "HILORE_ERR_UNSUPPORTED";
+    case HILORE_ERR_WORKSPACE: return "HILORE_ERR_WORKSPACE";
     case HILORE_ERR_HIP: return "HILORE_ERR_HIP";
     default: return "HILORE_ERR_UNKNOWN";
   }
@@ -276,6 +277,59 @@ hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, i
   a.N = N;
   a.accumulate = accumulate ? 1 : 0;
   return hip_status(hilore::launch_wgrad(a, code, block, static_cast<hipStream_t>(stream)));
+}
+
+size_t hilore_allocate_workspace_bytes(int n_units, int n_b, int n_d) {
+  if (n_units < 0 || n_units > hilore::kAllocMaxUnits || n_b < 1 || n_d < 1 ||
+      n_b > hilore::kAllocMaxIntervals || n_d > hilore::kAllocMaxIntervals)
+    return 0;
+  return hilore::alloc_layout(n_units, n_b + 1, n_d + 1).bytes;
+}
+
+hilore_status hilore_allocate(int n_units, const uint8_t *q, const uint8_t *verified,
+                              const double *tau_h, const double *tau_l, const double *dm_h,
+                              const double *dm_l, const double *psi, double m_res,
+                              double delta_b, int n_b, int n_d, uint8_t *action, double *totals,
+                              int64_t *jk, void *workspace, size_t workspace_bytes,
+                              void *stream) {
+  if (n_units < 0 || n_b < 1 || n_d < 1 || !(m_res >= 0.0) || !std::isfinite(m_res) ||
+      !(delta_b >= 0.0) || !std::isfinite(delta_b))
+    return HILORE_ERR_INVALID_ARG;
+  if (n_units > hilore::kAllocMaxUnits || n_b > hilore::kAllocMaxIntervals ||
+      n_d > hilore::kAllocMaxIntervals)
+    return HILORE_ERR_UNSUPPORTED;
+  if (!totals || !jk || !workspace) return HILORE_ERR_INVALID_ARG;
+  if (n_units > 0) {
+    const void *in[] = {q, verified, tau_h, tau_l, dm_h, dm_l, psi, action};
+    for (const void *p : in)
+      if (!p) return HILORE_ERR_INVALID_ARG;
+    const void *f64[] = {tau_h, tau_l, dm_h, dm_l, psi};
+    for (const void *p : f64)
+      if ((reinterpret_cast<uintptr_t>(p) & 7u) != 0) return HILORE_ERR_ALIGNMENT;
+  }
+  if ((reinterpret_cast<uintptr_t>(totals) & 7u) != 0 ||
+      (reinterpret_cast<uintptr_t>(jk) & 7u) != 0 || !aligned16(workspace))
+    return HILORE_ERR_ALIGNMENT;
+  const int KB = m_res > 0.0 ? n_b + 1 : 1;
+  const int KD = delta_b > 0.0 ? n_d + 1 : 1;
+  if (workspace_bytes < hilore::alloc_layout(n_units, KB, KD).bytes) return HILORE_ERR_WORKSPACE;
+  hilore::AllocArgs a{};
+  a.q = q;
+  a.verified = verified;
+  a.tau_h = tau_h;
+  a.tau_l = tau_l;
+  a.dm_h = dm_h;
+  a.dm_l = dm_l;
+  a.psi = psi;
+  a.m_res = m_res;
+  a.delta_b = delta_b;
+  a.U = n_units;
+  a.n_b = n_b;
+  a.n_d = n_d;
+  a.action = action;
+  a.totals = totals;
+  a.jk = jk;
+  return hip_status(hilore::launch_allocate(a, KB, KD, workspace, static_cast<hipStream_t>(stream)));
 }
 
 }  // extern "C"

@@ -1,0 +1,262 @@
+// Joint H/L/R recovery allocation on gfx950 (Sec. 3.4 Eq. joint-allocation,
+// solved as in App. B.2 Eqs. allocation-grid, allocation-integer-costs and
+// allocation-dp, with the available actions of App. B.3 Eq.
+// available-recovery-actions).
+//
+// Each unit u takes one action in {R, H, L}: R (recompute) is the baseline
+// with zero utility, memory and risk; H keeps the activation (utility tau_h,
+// memory dm_h, risk 0); L keeps its low-precision codes (tau_l, dm_l, risk
+// psi_u).  Memory and risk costs are rounded up to integer steps of the
+// budgets (N_B and N_delta intervals), and the dynamic programme
+//   F_i(j, k) = max over available a of F_{i-1}(j - b_i(a), k - r_i(a)) + tau_i(a)
+// runs over the (N_B + 1) x (N_delta + 1) grid of exact integer costs.
+//
+// Mapping.  One launch per unit updates the whole grid, one thread per cell
+// (rows k of risk cost, columns j of memory cost, a row padded to a multiple
+// of 64 cells so that a wave covers 64 consecutive cells of one row).  Each
+// cell reads its own value and the two shifted sources from the previous
+// table (fp64, all in the 256 MB infinity cache for grids up to a few
+// thousand squared) and writes its new value; the chosen action (2 bits) is
+// gathered across the wave with two ballots and stored as two 64-bit masks
+// per 64 cells, so the backtracking record of a 1025 x 1025 grid is 279 KB
+// per unit.  A reduction kernel then finds the best terminal cell, and a
+// single thread backtracks through the records and sums the chosen costs in
+// unit order.
+//
+// Every value is produced by the same fp64 operations in the same order as
+// a plain sequential implementation (one addition per unit along a path,
+// comparisons with the fixed tie rules), so actions and totals are exact.
+#include <math.h>
+
+#include "device_common.hpp"
+#include "hilore_internal.hpp"
+
+#pragma clang fp contract(off)
+
+namespace hilore {
+namespace {
+
+constexpr int kActR = 0, kActH = 1, kActL = 2;
+constexpr int kDpThreads = 256;
+constexpr int kPartials = 1024;  // workgroups of the terminal reduction
+constexpr int kFinalThreads = 1024;
+
+// Availability of a non-R action (App. B.3 Eq. available-recovery-actions;
+// non-R actions with non-positive utility are excluded, App. B.2): verified,
+// allowed by the retained representation q (H keeps everything, L excludes
+// H, R allows only R), and finite non-negative costs.
+__device__ bool action_ok(int act, uint8_t q, uint8_t verified, double tau, double dm,
+                          double risk) {
+  if (((verified >> act) & 1u) == 0) return false;
+  if (q == kActL && act == kActH) return false;
+  if (q != kActH && q != kActL) return false;
+  if (!(tau > 0.0) || !isfinite(tau)) return false;
+  if (!(dm >= 0.0) || !isfinite(dm)) return false;
+  if (!(risk >= 0.0) || !isfinite(risk)) return false;
+  return true;
+}
+
+// Integer cost on a grid of n intervals over `budget` (Eq.
+// allocation-integer-costs): ceil(cost / h) with h = budget / n, or n + 1
+// (does not fit) beyond n; with a zero budget only a zero cost fits.
+__device__ int64_t grid_cost(double cost, double budget, int n) {
+  if (!(budget > 0.0)) return cost == 0.0 ? 0 : (int64_t)n + 1;
+  const double h = budget / (double)n;
+  const double c = ceil(cost / h);
+  return c > (double)n ? (int64_t)n + 1 : (int64_t)c;
+}
+
+__global__ void costs_kernel(const AllocArgs a, AllocUnitCost *uc) {
+  const int u = blockIdx.x * blockDim.x + threadIdx.x;
+  if (u >= a.U) return;
+  const uint8_t q = a.q[u], v = a.verified[u];
+  int ok_h = action_ok(kActH, q, v, a.tau_h[u], a.dm_h[u], 0.0);
+  int ok_l = action_ok(kActL, q, v, a.tau_l[u], a.dm_l[u], a.psi[u]) && a.delta_b > 0.0;
+  const int64_t b_h = ok_h ? grid_cost(a.dm_h[u], a.m_res, a.n_b) : 0;
+  const int64_t b_l = ok_l ? grid_cost(a.dm_l[u], a.m_res, a.n_b) : 0;
+  const int64_t r_l = ok_l ? grid_cost(a.psi[u], a.delta_b, a.n_d) : 0;
+  if (b_h > a.n_b) ok_h = 0;
+  if (b_l > a.n_b || r_l > a.n_d) ok_l = 0;
+  AllocUnitCost c;
+  c.ok_h = ok_h;
+  c.ok_l = ok_l;
+  c.b_h = (int32_t)b_h;
+  c.b_l = (int32_t)b_l;
+  c.r_l = (int32_t)r_l;
+  c.pad = 0;
+  c.tau_h = a.tau_h[u];
+  c.tau_l = a.tau_l[u];
+  uc[u] = c;
+}
+
+// F_0: 0 at (0, 0), -inf elsewhere (padding cells included).
+__global__ void init_kernel(double *f, int64_t cells) {
+  const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
+  if (i < cells) f[i] = i == 0 ? 0.0 : -INFINITY;
+}
+
+// One unit of Eq. allocation-dp.  Actions are tried in the order R, H, L and
+// replace the incumbent only when strictly larger (the within-state tie
+// rule).  Padding cells (j >= KB) stay -inf.
+__global__ __launch_bounds__(kDpThreads) void dp_kernel(const double *__restrict__ prev,
+                                                         double *__restrict__ cur,
+                                                         uint64_t *__restrict__ pred,
+                                                         const AllocUnitCost *__restrict__ uc,
+                                                         int KB, int KD, int S) {
+  const int64_t cell = (int64_t)blockIdx.x * kDpThreads + threadIdx.x;
+  const int k = (int)(cell / S), j = (int)(cell % S);
+  if (k >= KD) return;  // whole waves: S and the grid are multiples of 64
+  const AllocUnitCost c = *uc;
+  double best = -INFINITY;
+  int act = kActR;
+  if (j < KB) {
+    best = prev[cell];
+    if (c.ok_h && c.b_h <= j) {
+      const double v = prev[cell - c.b_h] + c.tau_h;
+      if (v > best) {
+        best = v;
+        act = kActH;
+      }
+    }
+    if (c.ok_l && c.b_l <= j && c.r_l <= k) {
+      const double v = prev[cell - (int64_t)c.r_l * S - c.b_l] + c.tau_l;
+      if (v > best) {
+        best = v;
+        act = kActL;
+      }
+    }
+  }
+  cur[cell] = best;
+  const uint64_t lo = __ballot(act & 1);
+  const uint64_t hi = __ballot(act >> 1);
+  if ((threadIdx.x & (kWave - 1)) == 0) {
+    const int64_t w = cell / kWave;  // 64-cell chunk of this wave
+    pred[2 * w] = lo;
+    pred[2 * w + 1] = hi;
+  }
+}
+
+// The better of two terminal candidates: larger value, then the earlier cell
+// in (risk cost, memory cost) order, which is lower risk, then lower memory.
+__device__ __forceinline__ bool better(double v, int64_t i, double bv, int64_t bi) {
+  return v > bv || (v == bv && i < bi);
+}
+
+struct Best {
+  double v;
+  int64_t i;
+};
+
+template <int THREADS>
+__device__ Best block_best(Best b) {
+  __shared__ double sv[THREADS];
+  __shared__ int64_t si[THREADS];
+  sv[threadIdx.x] = b.v;
+  si[threadIdx.x] = b.i;
+  __syncthreads();
+  for (int off = THREADS / 2; off > 0; off >>= 1) {
+    if ((int)threadIdx.x < off && better(sv[threadIdx.x + off], si[threadIdx.x + off],
+                                         sv[threadIdx.x], si[threadIdx.x])) {
+      sv[threadIdx.x] = sv[threadIdx.x + off];
+      si[threadIdx.x] = si[threadIdx.x + off];
+    }
+    __syncthreads();
+  }
+  return Best{sv[0], si[0]};
+}
+
+__global__ __launch_bounds__(kDpThreads) void terminal_partial_kernel(const double *f,
+                                                                       int64_t cells,
+                                                                       Best *partial) {
+  Best b{-INFINITY, INT64_MAX};
+  for (int64_t i = (int64_t)blockIdx.x * kDpThreads + threadIdx.x; i < cells;
+       i += (int64_t)gridDim.x * kDpThreads) {
+    const double v = f[i];
+    if (better(v, i, b.v, b.i)) b = Best{v, i};
+  }
+  b = block_best<kDpThreads>(b);
+  if (threadIdx.x == 0) partial[blockIdx.x] = b;
+}
+
+__global__ __launch_bounds__(kFinalThreads) void terminal_backtrack_kernel(
+    const AllocArgs a, const Best *partial, int n_partial, const uint64_t *pred,
+    const AllocUnitCost *uc, int S, int KD) {
+  Best b{-INFINITY, INT64_MAX};
+  for (int p = threadIdx.x; p < n_partial; p += kFinalThreads)
+    if (better(partial[p].v, partial[p].i, b.v, b.i)) b = partial[p];
+  b = block_best<kFinalThreads>(b);
+  if (threadIdx.x != 0) return;
+  int64_t k = b.i / S, j = b.i % S;
+  a.jk[0] = j;
+  a.jk[1] = k;
+  a.totals[0] = b.v;
+  const int64_t chunks = S / kWave;
+  for (int i = a.U - 1; i >= 0; --i) {
+    const int64_t w = ((int64_t)i * KD + k) * chunks + j / kWave;
+    const int bit = (int)(j % kWave);
+    const int act = (int)((pred[2 * w] >> bit) & 1u) | ((int)((pred[2 * w + 1] >> bit) & 1u) << 1);
+    a.action[i] = (uint8_t)act;
+    if (act == kActH) j -= uc[i].b_h;
+    if (act == kActL) {
+      j -= uc[i].b_l;
+      k -= uc[i].r_l;
+    }
+  }
+  double mem = 0.0, risk = 0.0;
+  for (int i = 0; i < a.U; ++i) {
+    if (a.action[i] == kActH) mem += a.dm_h[i];
+    if (a.action[i] == kActL) {
+      mem += a.dm_l[i];
+      risk += a.psi[i];
+    }
+  }
+  a.totals[1] = mem;
+  a.totals[2] = risk;
+}
+
+}  // namespace
+
+AllocLayout alloc_layout(int U, int KB, int KD) {
+  auto up = [](size_t x) { return (x + 255) & ~size_t(255); };
+  AllocLayout l{};
+  l.S = (KB + kWave - 1) / kWave * kWave;
+  l.cells = (int64_t)l.S * KD;
+  l.off_costs = 0;
+  l.off_f0 = up(sizeof(AllocUnitCost) * (size_t)(U > 0 ? U : 1));
+  l.off_f1 = l.off_f0 + up(sizeof(double) * (size_t)l.cells);
+  l.off_partial = l.off_f1 + up(sizeof(double) * (size_t)l.cells);
+  l.off_pred = l.off_partial + up(sizeof(Best) * kPartials);
+  l.pred_bytes_per_unit = (size_t)(l.cells / kWave) * 16;
+  l.bytes = l.off_pred + up(l.pred_bytes_per_unit * (size_t)U);
+  return l;
+}
+
+hipError_t launch_allocate(const AllocArgs &a, int KB, int KD, void *workspace, hipStream_t s) {
+  const AllocLayout l = alloc_layout(a.U, KB, KD);
+  char *ws = static_cast<char *>(workspace);
+  AllocUnitCost *uc = reinterpret_cast<AllocUnitCost *>(ws + l.off_costs);
+  double *f[2] = {reinterpret_cast<double *>(ws + l.off_f0),
+                  reinterpret_cast<double *>(ws + l.off_f1)};
+  Best *partial = reinterpret_cast<Best *>(ws + l.off_partial);
+  uint64_t *pred = reinterpret_cast<uint64_t *>(ws + l.off_pred);
+
+  if (a.U > 0) {
+    hipLaunchKernelGGL(costs_kernel, dim3((a.U + 255) / 256), dim3(256), 0, s, a, uc);
+  }
+  const int grid = (int)((l.cells + kDpThreads - 1) / kDpThreads);
+  hipLaunchKernelGGL(init_kernel, dim3(grid), dim3(kDpThreads), 0, s, f[0], l.cells);
+  for (int i = 0; i < a.U; ++i) {
+    hipLaunchKernelGGL(dp_kernel, dim3(grid), dim3(kDpThreads), 0, s, f[i & 1], f[(i + 1) & 1],
+                       reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(pred) +
+                                                    l.pred_bytes_per_unit * (size_t)i),
+                       uc + i, KB, KD, l.S);
+  }
+  const int n_partial = grid < kPartials ? grid : kPartials;
+  hipLaunchKernelGGL(terminal_partial_kernel, dim3(n_partial), dim3(kDpThreads), 0, s,
+                     f[a.U & 1], l.cells, partial);
+  hipLaunchKernelGGL(terminal_backtrack_kernel, dim3(1), dim3(kFinalThreads), 0, s, a, partial,
+                     n_partial, pred, uc, l.S, KD);
+  return hipGetLastError();
+}
+
+}  // namespace hilore

@@ -97,4 +97,31 @@ struct WgradArgs {
 };
 hipError_t launch_wgrad(const WgradArgs &a, int code, int block, hipStream_t s);
 
+// Joint H/L/R allocation (App. B.2).  Per-unit arrays are device pointers.
+struct AllocArgs {
+  const uint8_t *q, *verified;
+  const double *tau_h, *tau_l, *dm_h, *dm_l, *psi;
+  double m_res, delta_b;
+  int U, n_b, n_d;
+  uint8_t *action;
+  double *totals;
+  int64_t *jk;
+};
+struct AllocUnitCost {  // integer costs of one unit on the grid
+  int32_t ok_h, ok_l;
+  int32_t b_h, b_l, r_l, pad;
+  double tau_h, tau_l;
+};
+struct AllocLayout {  // the caller's workspace, carved into 256-byte aligned parts
+  int S;              // cells per risk row (KB rounded up to 64)
+  int64_t cells;      // S * KD
+  size_t off_costs, off_f0, off_f1, off_partial, off_pred;
+  size_t pred_bytes_per_unit;
+  size_t bytes;
+};
+constexpr int kAllocMaxIntervals = 4096;   // N_B, N_delta at most
+constexpr int kAllocMaxUnits = 1 << 20;
+AllocLayout alloc_layout(int U, int KB, int KD);
+hipError_t launch_allocate(const AllocArgs &a, int KB, int KD, void *workspace, hipStream_t s);
+
 }  // namespace hilore

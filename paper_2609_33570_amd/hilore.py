@@ -19,6 +19,7 @@ HILORE_OK = 0
 HILORE_ERR_INVALID_ARG = 1
 HILORE_ERR_ALIGNMENT = 2
 HILORE_ERR_UNSUPPORTED = 3
+HILORE_ERR_WORKSPACE = 4
 HILORE_ERR_HIP = 5
 
 HILORE_CODE_INT8 = 0
@@ -73,6 +74,9 @@ def load() -> ctypes.CDLL:
         "hilore_decompress": (i32, [P, i32, i32, i32, P]),
         "hilore_unit_exposure_risk": (i32, [P, P, i64, P, i32, f32, f32, P, P, P, P]),
         "hilore_dequant_wgrad": (i32, [P, P, i32, i32, P, P, i64, i64, i64, i32, P]),
+        "hilore_allocate_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32]),
+        "hilore_allocate": (i32, [i32, P, P, P, P, P, P, P, f64, f64, i32, i32, P, P, P, P,
+                                  ctypes.c_size_t, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -177,3 +181,24 @@ def hilore_dequant_wgrad(x_codes, x_scales, code, block: int, dy, dw, K: int, M:
            load().hilore_dequant_wgrad(_p(x_codes), _p(x_scales), _code(code), int(block),
                                        _p(dy), _p(dw), int(K), int(M), int(N),
                                        1 if accumulate else 0, _stream(stream)))
+
+
+ACT_R, ACT_H, ACT_L = 0, 1, 2
+
+
+def hilore_allocate_workspace_bytes(n_units: int, n_b: int = 1024, n_d: int = 1024) -> int:
+    return int(load().hilore_allocate_workspace_bytes(int(n_units), int(n_b), int(n_d)))
+
+
+def hilore_allocate(q, verified, tau_h, tau_l, dm_h, dm_l, psi, m_res: float, delta_b: float,
+                    n_b: int, n_d: int, action, totals, jk, workspace, stream=None):
+    """Per-unit inputs and the outputs are device tensors (q, verified, action
+    uint8; tau/dm/psi and totals float64; jk int64); workspace is a device
+    tensor of at least hilore_allocate_workspace_bytes(...) bytes."""
+    n = int(q.numel())
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("hilore_allocate",
+           load().hilore_allocate(n, _p(q), _p(verified), _p(tau_h), _p(tau_l), _p(dm_h),
+                                  _p(dm_l), _p(psi), float(m_res), float(delta_b), int(n_b),
+                                  int(n_d), _p(action), _p(totals), _p(jk), _p(workspace),
+                                  ws_bytes, _stream(stream)))

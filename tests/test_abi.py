@@ -171,3 +171,50 @@ def test_wgrad_validation(lib):
     assert wgrad(lib, code=2, block=0, N=100) == E.HILORE_ERR_UNSUPPORTED
     assert wgrad(lib, code=2, block=0, x_scales=None, x_codes=FAKE + 1) == E.HILORE_ERR_ALIGNMENT
     assert wgrad(lib, code=2, block=0, x_scales=None, dy=None) == E.HILORE_ERR_INVALID_ARG
+
+
+def alloc(lib, **kw):
+    a = dict(U=4, q=FAKE, verified=FAKE, tau_h=FAKE, tau_l=FAKE, dm_h=FAKE, dm_l=FAKE, psi=FAKE,
+             m_res=1.0, delta_b=1.0, n_b=1024, n_d=1024, action=FAKE, totals=FAKE, jk=FAKE,
+             ws=FAKE, ws_bytes=None)
+    a.update(kw)
+    if a["ws_bytes"] is None:
+        a["ws_bytes"] = lib.hilore_allocate_workspace_bytes(a["U"], a["n_b"], a["n_d"]) - 1
+    return lib.hilore_allocate(a["U"], a["q"], a["verified"], a["tau_h"], a["tau_l"], a["dm_h"],
+                               a["dm_l"], a["psi"], a["m_res"], a["delta_b"], a["n_b"], a["n_d"],
+                               a["action"], a["totals"], a["jk"], a["ws"], a["ws_bytes"], None)
+
+
+def test_allocate_workspace_size(lib):
+    f = lib.hilore_allocate_workspace_bytes
+    one = f(1, 1024, 1024)
+    # two fp64 tables of 1025 rows x 1088 padded cells, and 2 bits per cell per unit
+    assert one >= 2 * 8 * 1025 * 1088 + 1025 * 1088 // 4
+    assert abs(f(11, 1024, 1024) - one - 10 * 1025 * 1088 // 4) < 256
+    assert f(0, 1, 1) > 0
+    assert f(-1, 1024, 1024) == 0 and f(1, 0, 1024) == 0 and f(1, 4097, 1024) == 0
+
+
+def test_allocate_validation(lib):
+    E = hilore
+    big = 1 << 40
+    # a workspace one byte short of what is needed
+    assert alloc(lib) == E.HILORE_ERR_WORKSPACE
+    assert alloc(lib, U=-1, ws_bytes=big) == E.HILORE_ERR_INVALID_ARG
+    assert alloc(lib, n_b=0, ws_bytes=big) == E.HILORE_ERR_INVALID_ARG
+    assert alloc(lib, n_d=0, ws_bytes=big) == E.HILORE_ERR_INVALID_ARG
+    assert alloc(lib, n_b=4097, ws_bytes=big) == E.HILORE_ERR_UNSUPPORTED
+    assert alloc(lib, m_res=-1.0, ws_bytes=big) == E.HILORE_ERR_INVALID_ARG
+    assert alloc(lib, delta_b=float("inf"), ws_bytes=big) == E.HILORE_ERR_INVALID_ARG
+    assert alloc(lib, delta_b=float("nan"), ws_bytes=big) == E.HILORE_ERR_INVALID_ARG
+    for name in ("q", "verified", "tau_h", "tau_l", "dm_h", "dm_l", "psi", "action", "totals",
+                 "jk", "ws"):
+        assert alloc(lib, ws_bytes=big, **{name: None}) == E.HILORE_ERR_INVALID_ARG, name
+    for name in ("tau_h", "psi", "totals", "jk"):
+        assert alloc(lib, ws_bytes=big, **{name: FAKE + 4}) == E.HILORE_ERR_ALIGNMENT, name
+    assert alloc(lib, ws_bytes=big, ws=FAKE + 8) == E.HILORE_ERR_ALIGNMENT
+    # per-unit arrays are not needed without units, but the outputs still are
+    assert alloc(lib, U=0, q=None, tau_h=None, totals=None, ws_bytes=big) == \
+        E.HILORE_ERR_INVALID_ARG
+    # zero budgets leave a single state per axis: a small workspace is checked too
+    assert alloc(lib, m_res=0.0, delta_b=0.0, ws_bytes=1000) == E.HILORE_ERR_WORKSPACE

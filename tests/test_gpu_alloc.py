@@ -1,0 +1,111 @@
+"""GPU parity of hilore_allocate (Sec. 3.4 Eq. joint-allocation on the grid of
+App. B.2) against the oracle's dynamic programme.
+
+Both sides evaluate the same fp64 operations in the same order (one addition
+per unit along a path, the fixed tie rules), so actions, totals and terminal
+costs must agree bit for bit: small random instances with real and integer
+utilities (many exact ties), coarse and fine grids, the 196-unit profiled
+Qwen2-7B-width plan on the paper's 1025 x 1025 grid, and the boundary cases
+(no units, zero memory and/or risk budget, nothing available).
+"""
+import numpy as np
+import pytest
+import torch
+
+from gpu_util import dev, host
+from paper_2609_33570_amd import workloads as wl
+
+pytestmark = pytest.mark.gpu
+
+
+def gpu_allocate(hl, inst, n_b, n_d, workspace=None):
+    U = inst.U
+    args = [dev(np.ascontiguousarray(a)) if U else torch.empty(0, device="cuda")
+            for a in (inst.q.astype(np.uint8), inst.verified.astype(np.uint8), inst.tau_h,
+                      inst.tau_l, inst.dm_h, inst.dm_l, inst.psi)]
+    action = torch.full((max(U, 1),), 0xEE, dtype=torch.uint8, device="cuda")
+    totals = torch.full((3,), float("nan"), dtype=torch.float64, device="cuda")
+    jk = torch.full((2,), -7, dtype=torch.int64, device="cuda")
+    need = hl.hilore_allocate_workspace_bytes(U, n_b, n_d)
+    if workspace is None:
+        # garbage on entry: the library must not depend on it
+        workspace = torch.randint(0, 255, (need,), dtype=torch.uint8, device="cuda")
+    q = args[0] if U else torch.empty(0, dtype=torch.uint8, device="cuda")
+    hl.hilore_allocate(q, *args[1:], inst.m_res, inst.delta_b, n_b, n_d, action, totals, jk,
+                       workspace)
+    torch.cuda.synchronize()
+    return host(action)[:U], host(totals), host(jk)
+
+
+def assert_same(got, want, what):
+    a, t, jk = got
+    oa, ot, ojk = want
+    assert np.array_equal(a, oa), (what, "actions", a, oa)
+    assert np.array_equal(t.view(np.uint64), ot.view(np.uint64)), (what, "totals", t, ot)
+    assert np.array_equal(jk, ojk), (what, "terminal costs", jk, ojk)
+
+
+def oracle_allocate(orc, inst, n_b, n_d):
+    return orc.allocate(*inst.arrays(), inst.m_res, inst.delta_b, n_b=n_b, n_d=n_d)
+
+
+@pytest.mark.parametrize("integer", [False, True], ids=["real", "integer"])
+@pytest.mark.parametrize("grid", [(1, 1), (3, 5), (16, 16), (64, 7), (1024, 1024)])
+def test_small_instances(hl, orc, integer, grid):
+    n_b, n_d = grid
+    for seed in range(12):
+        U = 1 + (seed * 5) % 14
+        inst = wl.alloc_small(U, seed=100 * seed + n_b + n_d, integer=integer, scale=8.0)
+        assert_same(gpu_allocate(hl, inst, n_b, n_d), oracle_allocate(orc, inst, n_b, n_d),
+                    f"U={U} seed={seed} grid={grid}")
+
+
+def test_profiled_plan_qwen2_7b(hl, orc):
+    """196 units (28 layers x 4 hidden + 3 MLP activations of a 16384-token
+    microbatch) on the 1025 x 1025 grid of the paper."""
+    inst = wl.alloc_instance(wl.qwen2_7b_unit_mix(), seed=wl.BASE_SEED + 3)
+    want = oracle_allocate(orc, inst, 1024, 1024)
+    got = gpu_allocate(hl, inst, 1024, 1024)
+    assert_same(got, want, "qwen2-7b plan")
+    assert (got[0] == 2).any() and (got[0] == 1).any(), "the plan should mix H and L"
+
+
+def test_boundaries(hl, orc):
+    base = wl.alloc_small(9, seed=5, scale=8.0)
+    cases = {
+        "zero memory": dict(m_res=0.0),
+        "zero risk": dict(delta_b=0.0),
+        "both zero": dict(m_res=0.0, delta_b=0.0),
+    }
+    for name, kw in cases.items():
+        inst = wl.AllocInstance(*base.arrays(), kw.get("m_res", base.m_res),
+                                kw.get("delta_b", base.delta_b))
+        for grid in ((1024, 1024), (4, 2)):
+            assert_same(gpu_allocate(hl, inst, *grid), oracle_allocate(orc, inst, *grid),
+                        f"{name} {grid}")
+    # zero-cost H units fit a zero memory budget
+    z = wl.AllocInstance(base.q, base.verified, base.tau_h, base.tau_l,
+                         np.where(np.arange(9) % 2 == 0, 0.0, base.dm_h), base.dm_l, base.psi,
+                         0.0, base.delta_b)
+    got = gpu_allocate(hl, z, 1024, 1024)
+    assert_same(got, oracle_allocate(orc, z, 1024, 1024), "zero-cost H")
+    # nothing available: all R, zero totals
+    r = wl.AllocInstance(np.zeros(9, np.uint8), *base.arrays()[1:], base.m_res, base.delta_b)
+    got = gpu_allocate(hl, r, 1024, 1024)
+    assert_same(got, oracle_allocate(orc, r, 1024, 1024), "all R")
+    assert not got[0].any() and not got[1].any()
+    # no units at all
+    e = wl.AllocInstance(*(a[:0] for a in base.arrays()), base.m_res, base.delta_b)
+    got = gpu_allocate(hl, e, 1024, 1024)
+    assert_same(got, oracle_allocate(orc, e, 1024, 1024), "no units")
+
+
+def test_workspace_reuse(hl, orc):
+    """Two calls in a row on one workspace, the second with fewer units and a
+    finer grid than the first left behind."""
+    ws = torch.empty(hl.hilore_allocate_workspace_bytes(40, 512, 512), dtype=torch.uint8,
+                     device="cuda")
+    a = wl.alloc_small(40, seed=11, scale=64.0)
+    b = wl.alloc_small(13, seed=12, scale=64.0)
+    assert_same(gpu_allocate(hl, a, 512, 512, ws), oracle_allocate(orc, a, 512, 512), "first")
+    assert_same(gpu_allocate(hl, b, 300, 500, ws), oracle_allocate(orc, b, 300, 500), "second")
