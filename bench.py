@@ -16,7 +16,9 @@ not hit the 256 MB infinity cache with the previous step's data.
 
 Prints ONE JSON line.  `value` is compress+decompress throughput in GB/s of
 algorithmic bytes (the first figure of the metric); the wgrad TFLOP/s and the
-coefficient tokens/s ride along, each with its own roofline.
+coefficient tokens/s ride along, each with its own roofline.  For context the
+line also times hilore_allocate (the H/L/R dynamic programme that follows the
+exposure step) on a 196-unit plan, outside the step.
 """
 from __future__ import annotations
 
@@ -47,6 +49,11 @@ def parse():
                    help="also time hipBLASLt's bf16 GEMM (torch.mm) on the reconstructed X, for context")
     p.add_argument("--cpu-rows", type=int, default=8192,
                    help="MLP rows (and 4x as many hidden rows) in the oracle's timed sample")
+    p.add_argument("--workload", default="qwen2_7b_layer",
+                   choices=["qwen2_7b_layer", "qwen2_7b_plan", "llama3_8b_stress"],
+                   help="qwen2_7b_layer: the full step with the 4096^3 wgrad (default); the "
+                        "others time coefficients + compress + exposure/risk + decompress of "
+                        "the whole-model plan (78 L units) or the Llama-3-8B-shaped stress case")
     return p.parse_args()
 
 
@@ -103,6 +110,8 @@ def main():
         print("no GPU visible", file=sys.stderr)
         return 1
     torch.cuda.set_device(0)
+    if args.workload != "qwen2_7b_layer":
+        return codec_workload(args, hl, wl)
 
     w = wl.QWEN2_7B_LAYER
     ww = wl.WGRAD_4096
@@ -265,6 +274,8 @@ def main():
         "rooflines": roofs,
     }
 
+    progress("timing the H/L/R allocation of a 196-unit plan")
+    out["allocate"] = alloc_bench(hl, wl)
     if args.blas_ref:
         progress("timing hipBLASLt on the reconstructed X")
         out["blas_ref"] = blas_ref(sets[0], code, block, K, M, N)
@@ -273,6 +284,182 @@ def main():
         out["cpu_baseline"] = cpu_baseline(args, sets[0], w, block, code)
     print(json.dumps(out))
     return 0
+
+
+def codec_workload(args, hl, wl):
+    """One step of the codec path over a multi-unit workload, in the order of
+    Algorithm 1: coefficients, batched compress with row sums, exposure/risk
+    of every L unit, batched decompress.  The working sets (23 GB and 75 GB)
+    are far beyond the caches, so no buffer rotation is needed."""
+    import numpy as np
+    import torch
+
+    import oracle  # noqa: F401  (imported for the CPU baseline only)
+
+    w = wl.WORKLOADS[args.workload]
+    code = hl.CODES[w.code]
+    block = w.block
+    if w.key == "qwen2_7b_plan":
+        act = wl.plan_actions(len(w.units), w.seed)
+        chosen = [i for i in range(len(w.units)) if act[i] == "L"]
+    else:
+        chosen = list(range(len(w.units)))
+    b = wl.grpo_batch(w.P, w.G, w.T, seed=w.seed, pad_frac=w.pad_frac)
+    R = w.P * w.G
+    slots = R * w.T
+    rows = w.units[0].rows
+    assert rows == slots, "coefficients are aligned 1:1 with activation rows"
+
+    def progress(msg):
+        print(f"[bench] {msg}", file=sys.stderr, flush=True)
+
+    progress(f"drawing {len(chosen)} units of {rows}x{w.units[0].cols} on the device")
+    rewards, lp_new, lp_old = (torch.from_numpy(a).cuda() for a in (b.rewards, b.logp_new,
+                                                                    b.logp_old))
+    mask = torch.from_numpy(b.mask).cuda() if b.mask is not None else None
+    adv = torch.empty(R, dtype=torch.float32, device="cuda")
+    flags = torch.empty(slots, dtype=torch.uint8, device="cuda")
+    coeff = torch.empty(slots, dtype=torch.float32, device="cuda")
+    ratio = torch.empty(slots, dtype=torch.float32, device="cuda")
+    keep, uc, ud = [], [], []
+    for i in chosen:
+        u = w.units[i]
+        x = wl.activation_device(u.rows, u.cols, w.seed * 1000 + i, dist=w.dist,
+                                 outliers=w.outliers)
+        codes = torch.empty((u.rows, u.cols), dtype=torch.uint8, device="cuda")
+        scales = torch.empty((u.rows, u.cols // block), dtype=torch.float32, device="cuda")
+        xhat = torch.empty((u.rows, u.cols), dtype=torch.bfloat16, device="cuda")
+        ssx = torch.empty(u.rows, dtype=torch.float32, device="cuda")
+        sse = torch.empty(u.rows, dtype=torch.float32, device="cuda")
+        keep.append((x, codes, scales, xhat, ssx, sse))
+        uc.append(hl.unit_desc(x=x, codes=codes, scales=scales, row_ss_x=ssx, row_ss_err=sse))
+        ud.append(hl.unit_desc(codes=codes, scales=scales, xhat=xhat))
+    n = len(chosen)
+    expo = torch.empty(n, dtype=torch.float32, device="cuda")
+    risk = torch.empty(n, dtype=torch.float32, device="cuda")
+    rel = torch.empty(n, dtype=torch.float32, device="cuda")
+    torch.cuda.synchronize()
+    names = ["grpo_coeffs", "compress", "exposure_risk", "decompress"]
+
+    def step(ev=None):
+        def mark(i):
+            if ev is not None:
+                ev[i].record()
+        mark(0)
+        hl.hilore_grpo_coeffs(rewards, lp_new, lp_old, None, mask, w.P, w.G, w.T, 0.2, 1e-6,
+                              0.0, 0.0, adv, ratio, flags, coeff)
+        mark(1)
+        hl.hilore_compress(uc, code, block)
+        mark(2)
+        hl.hilore_unit_exposure_risk(coeff, mask, rows, uc, 1e-8, 1e-8, expo, risk, rel)
+        mark(3)
+        hl.hilore_decompress(ud, code, block)
+        mark(4)
+
+    steps = min(args.steps, 5)
+    progress("warm-up")
+    for _ in range(max(1, min(args.warmup, 2))):
+        step()
+    torch.cuda.synchronize()
+    progress(f"timing {steps} steps")
+    events = [[torch.cuda.Event(enable_timing=True) for _ in range(5)] for _ in range(steps)]
+    t0 = time.perf_counter()
+    for i in range(steps):
+        step(events[i])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t0
+    avg = {nm: float(np.mean([ev[k].elapsed_time(ev[k + 1]) for ev in events]))
+           for k, nm in enumerate(names)}
+    comp_b = decomp_b = 0
+    for i in chosen:
+        c, d = codec_bytes(w.units[i].rows, w.units[i].cols, block, stats=True)
+        comp_b += c
+        decomp_b += d
+    codec_gbs = (comp_b + decomp_b) / ((avg["compress"] + avg["decompress"]) * 1e-3) / 1e9
+    grpo_bytes = slots * (4 + 4 + 4 + 4 + 1 + (1 if mask is not None else 0)) + R * 8
+    risk_bytes = rows * (4 + 4) * n + rows * (4 + (1 if mask is not None else 0))
+
+    def roof(name, nbytes):
+        a = nbytes / (avg[name] * 1e-3) / 1e9
+        return {"kernel": name, "bound": "hbm", "achieved": round(a, 2), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(a / HBM_PEAK_GBS, 4), "traffic": None,
+                "algorithmic": f"{nbytes} B per launch"}
+
+    roofs = {"compress": roof("compress", comp_b), "decompress": roof("decompress", decomp_b),
+             "grpo_coeffs": roof("grpo_coeffs", grpo_bytes),
+             "exposure_risk": roof("exposure_risk", risk_bytes)}
+    dominant = max(names, key=lambda k: avg[k])
+    out = {
+        "metric": METRIC, "value": round(codec_gbs, 2), "unit": "GB/s", "n_gpus": 1,
+        "steps": steps, "warmup": max(1, min(args.warmup, 2)),
+        "ms_per_step": round(wall / steps * 1e3, 4), "higher_is_better": True,
+        "scaling": "weak", "vs_baseline": None, "dtype": "bf16", "data": "synthetic",
+        "config": {"workload": w.key, "tokens": slots, "responses": R, "group": w.G,
+                   "units": [len(chosen), rows, w.units[0].cols], "code": w.code,
+                   "block": block, "padded_frac": None if b.mask is None else
+                   round(1.0 - float(b.mask.mean()), 4)},
+        "codec_frac_hbm": round(codec_gbs / HBM_PEAK_GBS, 4),
+        "coeff_tok_s": round(slots / (avg["grpo_coeffs"] * 1e-3), 1),
+        "kernel_ms": {k: round(v, 5) for k, v in avg.items()},
+        "roofline": roofs[dominant], "rooflines": roofs,
+    }
+    if not args.no_cpu_baseline:
+        progress("timing the oracle on the host")
+        import oracle
+
+        oracle.lib()
+        n_rows = min(rows, 4096)
+        x = keep[0][0][:n_rows].cpu().contiguous().view(torch.int16).numpy().view(np.uint16)
+        t0 = time.perf_counter()
+        c, sc = oracle.quantize(x, code, block)
+        xh = oracle.dequantize(c, sc, code, block)
+        oracle.row_stats(x, xh)
+        dt = time.perf_counter() - t0
+        cb, db = codec_bytes(n_rows, x.shape[1], block, stats=True)
+        out["cpu_baseline"] = {"value": round((cb + db) / dt / 1e9, 4), "unit": "GB/s",
+                               "cores": 1, "kind": "oracle",
+                               "sample": f"compress+decompress of {n_rows}x{x.shape[1]} rows of "
+                                         f"the first unit ({w.code} 1x{block}); {dt:.1f} s"}
+    print(json.dumps(out))
+    return 0
+
+
+def alloc_bench(hl, wl, iters=10):
+    """Context: hilore_allocate on the profiled plan of a Qwen2-7B-width model
+    (28 layers x 7 saved activations of a 16384-token microbatch = 196 units)
+    on the paper's 1025 x 1025 grid; per-unit inputs already on the device."""
+    import numpy as np
+    import torch
+
+    inst = wl.alloc_instance(wl.qwen2_7b_unit_mix(), seed=wl.BASE_SEED + 3)
+    n_b = n_d = 1024
+    d = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in inst.arrays()]
+    action = torch.empty(inst.U, dtype=torch.uint8, device="cuda")
+    totals = torch.empty(3, dtype=torch.float64, device="cuda")
+    jk = torch.empty(2, dtype=torch.int64, device="cuda")
+    ws = torch.empty(hl.hilore_allocate_workspace_bytes(inst.U, n_b, n_d), dtype=torch.uint8,
+                     device="cuda")
+
+    def call():
+        hl.hilore_allocate(*d, inst.m_res, inst.delta_b, n_b, n_d, action, totals, jk, ws)
+
+    for _ in range(2):
+        call()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(iters):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / iters
+    a = action.cpu().numpy()
+    cells = (n_b + 1) * ((n_b + 1 + 63) // 64 * 64)
+    return {"units": inst.U, "grid": [n_b + 1, n_d + 1], "ms": round(ms, 4),
+            "us_per_unit": round(ms * 1e3 / inst.U, 3),
+            "table_bytes_per_unit": cells * 16 + cells // 4,
+            "chosen": {"R": int((a == 0).sum()), "H": int((a == 1).sum()),
+                       "L": int((a == 2).sum())}}
 
 
 def blas_ref(st, code, block, K, M, N, iters=10):
@@ -340,6 +527,12 @@ def cpu_baseline(args, st, w, block, code):
     t0 = time.perf_counter()
     oracle.wgrad(wc, ws, code, block, dy, variant=0)
     dt_w = time.perf_counter() - t0
+    from paper_2609_33570_amd import workloads as wl
+
+    inst = wl.alloc_instance(wl.qwen2_7b_unit_mix(), seed=wl.BASE_SEED + 3)
+    t0 = time.perf_counter()
+    oracle.allocate(*inst.arrays(), inst.m_res, inst.delta_b, n_b=1024, n_d=1024)
+    dt_alloc = time.perf_counter() - t0
     return {
         "value": round(total / dt_codec / 1e9, 4),
         "unit": "GB/s",
@@ -351,6 +544,8 @@ def cpu_baseline(args, st, w, block, code):
         "coeff_tok_s": round(b.P * b.G * b.T / dt_grpo, 1),
         "wgrad_tflops": round(2.0 * K * 128 * 128 / dt_w / 1e12, 6),
         "wgrad_sample": f"dW[0:128, 0:128] over K={K} in fp64, {dt_w:.1f} s",
+        "allocate_ms": round(dt_alloc * 1e3, 1),
+        "allocate_sample": "the same 196-unit plan on the 1025 x 1025 grid",
     }
 
 
