@@ -32,13 +32,17 @@
 // Per stage LDS holds 32 KB of each operand; two stages in flight (128 KB of
 // the 160 KB).
 //
-// Pipeline per stage s (four k-step regions of 8 MFMAs per wave): region 0
-// starts the DMA of stage s+1's dY into the other buffer; regions 2 and 3
-// dequantise stage s+1's X (already in registers) into that buffer, and
-// region 3 then issues the global loads of stage s+2's X into the same
-// registers.  Every region reads the next k-step's fragments while its
-// MFMAs issue.  A wait for this thread's DMA and one barrier end the stage.
-//
+// Pipeline per stage s (four k-step regions of 8 MFMAs per wave): regions 1
+// and 2 dequantise stage s+1's X (already in registers) into the other
+// buffer, and region 2 then issues the global loads of stage s+2's X into
+// the same registers.  Each thread waits for its own DMA of stage s+1's dY
+// and one barrier publishes stage s+1 before the last region, so that
+// region 3 finds its fragments in registers: while its MFMAs issue it
+// starts the DMA of stage s+2's dY into the buffer just finished and reads
+// stage s+1's first fragments, and no wave waits on LDS after the barrier.
+// Within a stage every region reads the next k-step's fragments while its
+// MFMAs issue; B fragments alternate between two register sets, so the next
+// k-step's B is requested right after the first MFMA.
 // Work distribution: workgroups are dealt round-robin to the 8 XCDs; the
 // launch index is remapped so that each XCD receives a contiguous run of
 // tiles, and runs are laid out 8 tile-rows tall, so the 32 CUs of an XCD share
@@ -188,8 +192,11 @@ __device__ __forceinline__ void fill_x(const Stage &st, uint8_t *a_lds, int lc, 
   *reinterpret_cast<u32x4 *>(a_lds + lds_off(lc * 4 + C + 1, g)) = p;
 }
 
+// A fragments of one k-step; B fragments of two (k-steps alternate between
+// the two sets, so the next k-step's B can be read while this one's MFMAs
+// still use theirs).
 struct Frags {
-  bf16x8 a[4], b[2];
+  bf16x8 a[4], b[2][2];
 };
 
 typedef short s16x4 __attribute__((ext_vector_type(4)));
@@ -208,98 +215,90 @@ struct FragPlan {
 
 // MFMA operands of k-step KS (t = 16 KS .. 16 KS + 15) for this wave.
 template <int KS>
+__device__ __forceinline__ bf16x8 read_b(const uint8_t *bl, const FragPlan &fp, int j) {
+  const s16x4 lo = read_tr16(bl + fp.yb[j] + KS * 16 * 512);
+  const s16x4 hi = read_tr16(bl + fp.yb[j] + (KS * 16 + 4) * 512);
+  return __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
+}
+
+template <int KS>
 __device__ __forceinline__ void read_frags(Frags &f, const uint8_t *al, const uint8_t *bl,
                                            const FragPlan &fp) {
 #pragma unroll
+  for (int j = 0; j < 2; ++j) f.b[KS & 1][j] = read_b<KS>(bl, fp, j);
+#pragma unroll
   for (int i = 0; i < 4; ++i)
     f.a[i] = *reinterpret_cast<const bf16x8 *>(
         al + lds_off(fp.wm * 128 + i * 32 + fp.lrow, KS * 2 + fp.lk));
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const s16x4 lo = read_tr16(bl + fp.yb[j] + KS * 16 * 512);
-    const s16x4 hi = read_tr16(bl + fp.yb[j] + (KS * 16 + 4) * 512);
-    f.b[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
-  }
 }
 
-__device__ __forceinline__ void mma8(f32x16 (&acc)[4][2], const Frags &f) {
-#pragma unroll
-  for (int i = 0; i < 4; ++i)
-#pragma unroll
-    for (int j = 0; j < 2; ++j)
-      acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[j], acc[i][j], 0, 0, 0);
-}
-
-// The 8 MFMAs of this k-step with the fragment reads of k-step KS woven in:
-// each A fragment is re-read as soon as its two MFMAs have been issued, the
-// B fragments after the last one, so the reads start up to six MFMAs
-// earlier than after the whole block.
+// The 8 MFMAs of this k-step (B fragments in set (KS + 3) % 2, i.e. the set
+// of k-step KS - 1) with the fragment reads of k-step KS woven in: the B
+// fragments of k-step KS go to the other set right after the first MFMA, and
+// each A fragment is re-read as soon as its two MFMAs have been issued.
 template <int KS>
 __device__ __forceinline__ void mma8_read(f32x16 (&acc)[4][2], Frags &f, const uint8_t *al,
                                           const uint8_t *bl, const FragPlan &fp) {
+  constexpr int CUR = (KS + 1) & 1, NXT = KS & 1;
+#pragma unroll
+  for (int j = 0; j < 2; ++j) f.b[NXT][j] = read_b<KS>(bl, fp, j);
 #pragma unroll
   for (int i = 0; i < 4; ++i) {
-    acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[0], acc[i][0], 0, 0, 0);
-    acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[1], acc[i][1], 0, 0, 0);
+    acc[i][0] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[CUR][0], acc[i][0], 0, 0, 0);
+    acc[i][1] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(f.a[i], f.b[CUR][1], acc[i][1], 0, 0, 0);
     f.a[i] = *reinterpret_cast<const bf16x8 *>(
         al + lds_off(fp.wm * 128 + i * 32 + fp.lrow, KS * 2 + fp.lk));
-  }
-#pragma unroll
-  for (int j = 0; j < 2; ++j) {
-    const s16x4 lo = read_tr16(bl + fp.yb[j] + KS * 16 * 512);
-    const s16x4 hi = read_tr16(bl + fp.yb[j] + (KS * 16 + 4) * 512);
-    f.b[j] = __builtin_bit_cast(bf16x8, __builtin_shufflevector(lo, hi, 0, 1, 2, 3, 4, 5, 6, 7));
   }
 }
 
 // Instruction order of one k-step region: every MFMA followed by VALU ops
-// of the next stage's dequantisation (last two regions), LDS stores spread
+// of the next stage's dequantisation (regions 1 and 2), LDS stores spread
 // over the region, global loads after the first MFMAs, and the LDS reads of
-// the next k-step's fragments: one A fragment after every second MFMA, the
-// rest after the last.
+// the next k-step's fragments: the four B reads after the first MFMA, one A
+// fragment after every second MFMA.
 template <bool NEXT, int VALU, int WRITES, int LOADS>
 __device__ __forceinline__ void schedule_region() {
 #pragma unroll
   for (int i = 0; i < 8; ++i) {
     __builtin_amdgcn_sched_group_barrier(0x008, 1, 0);  // 1 MFMA
+    if constexpr (NEXT)
+      if (i == 0) __builtin_amdgcn_sched_group_barrier(0x100, 4, 0);
     if constexpr (VALU > 0) __builtin_amdgcn_sched_group_barrier(0x002, VALU, 0);
     if constexpr (WRITES > 0)
       if (i % (8 / WRITES) == 8 / WRITES - 1) __builtin_amdgcn_sched_group_barrier(0x200, 1, 0);
     if constexpr (LOADS > 0)
       if (i < (LOADS + 1) / 2) __builtin_amdgcn_sched_group_barrier(0x020, 2, 0);
     if constexpr (NEXT)
-      if (i == 1 || i == 3 || i == 5) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
+      if (i & 1) __builtin_amdgcn_sched_group_barrier(0x100, 1, 0);
   }
-  if constexpr (NEXT) __builtin_amdgcn_sched_group_barrier(0x100, 5, 0);  // 5 more LDS reads
   __builtin_amdgcn_sched_barrier(0);
 }
 
-// One k-step region of a stage.  Region 0 starts the DMA of the next
-// stage's dY; regions 2 and 3 dequantise the next stage's X into the other
-// LDS buffer, and region 3 then issues the global loads of the stage after
-// that into the same registers (so one register set suffices and the loads
-// have until region 2 of the next stage to land).  The fragments of the next
-// k-step are read into the same registers once this k-step's MFMAs have been
-// issued (each A fragment as soon as its MFMAs are); the other wave on the
-// SIMD covers the rest of that latency.
+// One k-step region of a stage s.  Regions 1 and 2 dequantise stage s+1's
+// X (already in registers) into the other LDS buffer; region 2 then issues
+// the global loads of stage s+2's X into the same registers.  The barrier
+// that publishes stage s+1 sits between regions 2 and 3, so region 3 can
+// start the DMA of stage s+2's dY into this stage's buffer (no wave reads
+// it any more) and read stage s+1's first fragments while its own MFMAs
+// issue: no wave waits on LDS after the barrier.
 template <int CODE, int KS>
 __device__ __forceinline__ void region(f32x16 (&acc)[4][2], Frags &f, const uint8_t *cur_a,
-                                       const uint8_t *cur_b, uint8_t *nxt_a, uint8_t *nxt_b,
+                                       uint8_t *cur_b, uint8_t *nxt_a, uint8_t *nxt_b,
                                        Stage &raw, __amdgpu_buffer_rsrc_t ry, const XRsrc &rx,
                                        const LoadPlan &lp, const FragPlan &fp, int wave, int lc,
                                        int g) {
-  if constexpr (KS == 0) dma_dy(ry, lp, nxt_b, wave);
-  if constexpr (KS == 2) fill_x<CODE, 0>(raw, nxt_a, lc, g);
-  if constexpr (KS == 3) {
+  if constexpr (KS == 1) fill_x<CODE, 0>(raw, nxt_a, lc, g);
+  if constexpr (KS == 2) {
     fill_x<CODE, 2>(raw, nxt_a, lc, g);
     load_stage<CODE>(raw, rx, lp);
   }
+  if constexpr (KS == 3) dma_dy(ry, lp, cur_b, wave);
   if constexpr (KS < 3) mma8_read<KS + 1>(acc, f, cur_a, cur_b, fp);
-  if constexpr (KS == 3) mma8(acc, f);
-  if constexpr (KS == 0) schedule_region<true, 0, 0, kYLoads>();
-  if constexpr (KS == 1) schedule_region<true, 0, 0, 0>();
-  if constexpr (KS == 2) schedule_region<true, 4, 2, 0>();
-  if constexpr (KS == 3) schedule_region<false, 4, 2, kXLoads<CODE>>();
+  if constexpr (KS == 3) mma8_read<0>(acc, f, nxt_a, nxt_b, fp);
+  if constexpr (KS == 0) schedule_region<true, 0, 0, 0>();
+  if constexpr (KS == 1) schedule_region<true, 4, 2, 0>();
+  if constexpr (KS == 2) schedule_region<true, 4, 2, kXLoads<CODE>>();
+  if constexpr (KS == 3) schedule_region<true, 0, 0, kYLoads>();
 }
 
 // s_waitcnt with only the vector-memory count limited (expcnt and lgkmcnt
@@ -310,26 +309,25 @@ __device__ __forceinline__ void wait_vmcnt() {
   __builtin_amdgcn_s_waitcnt((N & 15) | ((N >> 4) << 14) | (7 << 4) | (15 << 8));
 }
 
-// A full stage: MFMAs on `cur`, the next stage's dY (DMA) and X (from `raw`)
-// into `nxt`, then the loads of the stage after that into `raw`.  Before the
-// barrier every thread waits for its own DMA (the X loads issued after it
-// may stay in flight); the barrier then publishes the whole tile.
+// A full stage s on `cur` (its first fragments already in f): stage s+1's X
+// from `raw` into `nxt`, the loads of stage s+2's X into `raw`, the barrier
+// (each thread first waits for its own DMA of stage s+1's dY; the X loads
+// issued after it may stay in flight), then the last k-step, the DMA of stage
+// s+2's dY into `cur` and the first fragments of stage s+1 from `nxt`.
 template <int CODE, int BLOCK>
-__device__ __forceinline__ void stage(f32x16 (&acc)[4][2], const uint8_t *cur_a,
-                                      const uint8_t *cur_b, uint8_t *nxt_a, uint8_t *nxt_b,
-                                      Stage &raw, const WgradArgs &a, int64_t k_next,
+__device__ __forceinline__ void stage(f32x16 (&acc)[4][2], Frags &f, const uint8_t *cur_a,
+                                      uint8_t *cur_b, uint8_t *nxt_a, uint8_t *nxt_b,
+                                      Stage &raw, const WgradArgs &a, int64_t k_next2,
                                       const LoadPlan &lp, const FragPlan &fp, int wave, int lc,
                                       int g) {
-  const __amdgpu_buffer_rsrc_t ry = y_rsrc(a, k_next);
-  const XRsrc rx = x_rsrc<BLOCK>(a, k_next + BK);
-  Frags f;
-  read_frags<0>(f, cur_a, cur_b, fp);
+  const __amdgpu_buffer_rsrc_t ry = y_rsrc(a, k_next2);
+  const XRsrc rx = x_rsrc<BLOCK>(a, k_next2);
   region<CODE, 0>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
   region<CODE, 1>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
   region<CODE, 2>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
-  region<CODE, 3>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
   wait_vmcnt<kXLoads<CODE>>();
   __syncthreads();
+  region<CODE, 3>(acc, f, cur_a, cur_b, nxt_a, nxt_b, raw, ry, rx, lp, fp, wave, lc, g);
 }
 
 template <int CODE, int BLOCK>
@@ -408,19 +406,22 @@ __global__ __launch_bounds__(kThreads, 1) void wgrad_kernel(const WgradArgs a, i
   // constant.
   const int64_t n_stages = ((a.K + BK - 1) / BK + 1) & ~int64_t(1);
   Stage raw;
+  Frags f;
   dma_dy(y_rsrc(a, 0), lp, lds_b0, wave);
   load_stage<CODE>(raw, x_rsrc<BLOCK>(a, 0), lp);
   fill_x<CODE, 0>(raw, lds_a0, lc, g);
   fill_x<CODE, 2>(raw, lds_a0, lc, g);
   load_stage<CODE>(raw, x_rsrc<BLOCK>(a, BK), lp);
-  wait_vmcnt<kXLoads<CODE>>();
+  dma_dy(y_rsrc(a, BK), lp, lds_b1, wave);
+  wait_vmcnt<kXLoads<CODE> + kYLoads>();
   __syncthreads();
+  read_frags<0>(f, lds_a0, lds_b0, fp);
 
   for (int64_t s = 0; s < n_stages; s += 2) {
-    stage<CODE, BLOCK>(acc, lds_a0, lds_b0, lds_a1, lds_b1, raw, a, (s + 1) * BK, lp, fp, wave,
-                       lc, g);
-    stage<CODE, BLOCK>(acc, lds_a1, lds_b1, lds_a0, lds_b0, raw, a, (s + 2) * BK, lp, fp, wave,
-                       lc, g);
+    stage<CODE, BLOCK>(acc, f, lds_a0, lds_b0, lds_a1, lds_b1, raw, a, (s + 2) * BK, lp, fp,
+                       wave, lc, g);
+    stage<CODE, BLOCK>(acc, f, lds_a1, lds_b1, lds_a0, lds_b0, raw, a, (s + 3) * BK, lp, fp,
+                       wave, lc, g);
   }
 
   // Epilogue.  32x32 accumulator layout: lane l holds column l % 32 and, for
