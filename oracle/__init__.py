@@ -74,6 +74,10 @@ def lib() -> ctypes.CDLL:
             "orc_wgrad_entries": (None, [P, P, i32, i32, P, i64, i64, i64, P, P, i64, i32, P]),
             "orc_allocate": (i32, [i32, P, P, P, P, P, P, P, f64, f64, i32, i32, P, P, P]),
             "orc_allocate_brute": (i32, [i32, P, P, P, P, P, P, P, f64, f64, i32, i32, P, P, P]),
+            "orc_grad_rel_err": (f64, [P, P, i64, f64]),
+            "orc_calibrate": (None, [i32, i32, i32, P, P, P, P, P, P]),
+            "orc_risk_score": (None, [i32, P, i32, P, P, P, P]),
+            "orc_update_sparsity": (f64, [P, P, P, P, i32, i32, f64, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -267,3 +271,50 @@ def allocate(q, verified, tau_h, tau_l, dm_h, dm_l, psi, m_res, delta_b, n_b=102
     if rc != 0:
         raise ValueError("invalid allocation arguments")
     return action[:U], totals, jk
+
+
+# ------------------------------------------------- calibration and diagnostics --
+def grad_rel_err(g_l, g_ex, eps_num=1e-30):
+    """y = sqrt(||g_l - g_ex||^2 / max(||g_ex||^2, eps_num)) over fp32 values, fp64 sums."""
+    a = _c(g_l, np.float32).ravel()
+    b = _c(g_ex, np.float32).ravel()
+    assert a.size == b.size
+    return lib().orc_grad_rel_err(_ptr(a), _ptr(b), a.size, float(eps_num))
+
+
+def calibrate(unit_class, exposure, rel_err, grad_err, n_classes):
+    """exposure, rel_err, grad_err: [n_batches, n_units] (fp32 values).
+    Returns (kappa f64[n_classes], ebar f64[n_units])."""
+    cls = _c(unit_class, np.int32).ravel()
+    e = _c(exposure, np.float32)
+    r = _c(rel_err, np.float32)
+    y = _c(grad_err, np.float32)
+    nb, nu = e.shape
+    assert cls.size == nu and r.shape == e.shape and y.shape == e.shape
+    kappa = np.empty(max(n_classes, 1), dtype=np.float64)
+    ebar = np.empty(max(nu, 1), dtype=np.float64)
+    lib().orc_calibrate(nu, nb, int(n_classes), _ptr(cls), _ptr(e), _ptr(r), _ptr(y),
+                        _ptr(kappa), _ptr(ebar))
+    return kappa[:n_classes], ebar[:nu]
+
+
+def risk_score(unit_class, kappa, ebar, exposure):
+    cls = _c(unit_class, np.int32).ravel()
+    k = _c(kappa, np.float64).ravel()
+    eb = _c(ebar, np.float64).ravel()
+    e = _c(exposure, np.float32).ravel()
+    psi = np.empty(max(cls.size, 1), dtype=np.float64)
+    lib().orc_risk_score(cls.size, _ptr(cls), k.size, _ptr(k), _ptr(eb), _ptr(e), _ptr(psi))
+    return psi[:cls.size]
+
+
+def update_sparsity(coeff, flags, adv, mask, R, T, top_frac=0.1):
+    """Returns (counts i64[3] = padding, zero-advantage, clipped slots; top-k share)."""
+    w = _c(coeff, np.float64).ravel()
+    f = _c(flags, np.uint8).ravel()
+    a = _c(adv, np.float32).ravel()
+    m = _c(mask, np.uint8)
+    counts = np.zeros(3, dtype=np.int64)
+    share = lib().orc_update_sparsity(_ptr(w), _ptr(f), _ptr(a), None if m is None else _ptr(m.ravel()),
+                                      int(R), int(T), float(top_frac), _ptr(counts))
+    return counts, share

@@ -639,3 +639,110 @@ int orc_allocate_brute(int U, const uint8_t *q, const uint8_t *verified, const d
   totals[2] = risk;
   return 0;
 }
+
+/* ======================================================================= */
+/* Calibration scalars and update diagnostics                              */
+/* ======================================================================= */
+
+/* Relative gradient error of one single-unit L intervention (App. B.1 Eq.
+ * app-calibration-error, the y of Sec. 3.4 Eq. calibration-metrics): both
+ * gradients are taken as fp32 values, the norms in fp64,
+ *   y = sqrt( ||g_l - g_ex||^2 / max(||g_ex||^2, eps_num) ). */
+double orc_grad_rel_err(const float *g_l, const float *g_ex, int64_t n, double eps_num) {
+  double num = 0.0, den = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    const double d = (double)g_l[i] - (double)g_ex[i];
+    num += d * d;
+    den += (double)g_ex[i] * (double)g_ex[i];
+  }
+  return sqrt(num / (den > eps_num ? den : eps_num));
+}
+
+/* Susceptibility and mean reconstruction error from calibration passes
+ * (App. B.1 Eqs. app-kappa, app-risk-score; Sec. 3.4 Eq. susceptibility).
+ * Per calibration microbatch b and unit u the inputs hold the exposure E, the
+ * reconstruction error e^L and the measured gradient error y, row b of each
+ * [n_batches][n_units] array.  With x = E * e^L, the class-c least-squares fit
+ * of y = kappa x over kappa >= 0 has the closed form
+ *   kappa_c = max(0, sum x y / sum x^2)   (0 when sum x^2 = 0),
+ * the sums running over the (u, b) with class(u) = c; units whose class is
+ * outside [0, n_classes) take no part.  ebar_u = (1/n_batches) sum_b e^L_{u,b}. */
+void orc_calibrate(int n_units, int n_batches, int n_classes, const int32_t *unit_class,
+                   const float *exposure, const float *rel_err, const float *grad_err,
+                   double *kappa, double *ebar) {
+  for (int c = 0; c < n_classes; ++c) {
+    double sxy = 0.0, sxx = 0.0;
+    for (int b = 0; b < n_batches; ++b)
+      for (int u = 0; u < n_units; ++u) {
+        if (unit_class[u] != c) continue;
+        const int64_t i = (int64_t)b * n_units + u;
+        const double x = (double)exposure[i] * (double)rel_err[i];
+        sxy += x * (double)grad_err[i];
+        sxx += x * x;
+      }
+    const double k = sxx > 0.0 ? sxy / sxx : 0.0;
+    kappa[c] = k > 0.0 ? k : 0.0;
+  }
+  for (int u = 0; u < n_units; ++u) {
+    double s = 0.0;
+    for (int b = 0; b < n_batches; ++b) s += (double)rel_err[(int64_t)b * n_units + u];
+    ebar[u] = n_batches > 0 ? s / (double)n_batches : 0.0;
+  }
+}
+
+/* Calibrated risk of each unit's L action (App. B.1 Eq. app-risk-score):
+ *   psi_u = kappa_{c(u)} * E_u * ebar_u,
+ * multiplied in that order in fp64.  A unit without a class (outside
+ * [0, n_classes)) has no calibration: psi = +inf, which makes L unavailable
+ * to the allocator. */
+void orc_risk_score(int n_units, const int32_t *unit_class, int n_classes, const double *kappa,
+                    const double *ebar, const float *exposure, double *psi) {
+  for (int u = 0; u < n_units; ++u) {
+    const int c = unit_class[u];
+    psi[u] = (c >= 0 && c < n_classes) ? kappa[c] * (double)exposure[u] * ebar[u] : INFINITY;
+  }
+}
+
+static int cmp_desc(const void *a, const void *b) {
+  const double x = *(const double *)a, y = *(const double *)b;
+  return x < y ? 1 : (x > y ? -1 : 0);
+}
+
+/* Structural sparsity of one batch of update coefficients (the diagnostic
+ * replays of App. D.3, Policy-Update Exposure Details): over the n = R*T
+ * response slots (padding included), the slots whose policy gradient is zero
+ * for each exclusive cause,
+ *   counts[0] padding (m = 0),
+ *   counts[1] valid slots of a zero-advantage response,
+ *   counts[2] valid nonzero-advantage slots on the clipped, flat branch
+ *             (flag bit 1 of the coefficient step),
+ * and the share of sum |omega| held by the k = max(1, ceil(top_frac * n))
+ * largest |omega| (padding counted as 0; 0 when every omega is 0).  The sort
+ * puts the largest first, so ties do not change the sum. */
+double orc_update_sparsity(const double *coeff, const uint8_t *flags, const float *adv,
+                           const uint8_t *mask, int R, int T, double top_frac, int64_t *counts) {
+  const int64_t n = (int64_t)R * T;
+  counts[0] = counts[1] = counts[2] = 0;
+  double *mag = (double *)malloc((size_t)(n > 0 ? n : 1) * sizeof(double));
+  double total = 0.0;
+  for (int64_t i = 0; i < n; ++i) {
+    const int valid = mask ? mask[i] != 0 : 1;
+    if (!valid) counts[0] += 1;
+    else if (adv[i / T] == 0.0f) counts[1] += 1;
+    else if (flags[i] & 2) counts[2] += 1;
+    mag[i] = valid ? fabs(coeff[i]) : 0.0;
+    total += mag[i];
+  }
+  double share = 0.0;
+  if (n > 0 && total > 0.0) {
+    int64_t k = (int64_t)ceil(top_frac * (double)n);
+    if (k < 1) k = 1;
+    if (k > n) k = n;
+    qsort(mag, (size_t)n, sizeof(double), cmp_desc);
+    double top = 0.0;
+    for (int64_t i = 0; i < k; ++i) top += mag[i];
+    share = top / total;
+  }
+  free(mag);
+  return share;
+}

@@ -107,6 +107,24 @@ int orc_allocate_brute(int U, const uint8_t *q, const uint8_t *verified, const d
                        const double *psi, double m_res, double delta_b, int n_b, int n_d,
                        uint8_t *action, double *totals, int64_t *jk);
 
+/* ---- calibration scalars (App. B.1 Eqs. app-calibration-error, app-kappa,
+ *      app-risk-score; Sec. 3.4 Eqs. calibration-metrics, susceptibility) ---- */
+double orc_grad_rel_err(const float *g_l, const float *g_ex, int64_t n, double eps_num);
+/* exposure, rel_err, grad_err: fp32 [n_batches][n_units]; kappa f64 [n_classes],
+ * ebar f64 [n_units] */
+void orc_calibrate(int n_units, int n_batches, int n_classes, const int32_t *unit_class,
+                   const float *exposure, const float *rel_err, const float *grad_err,
+                   double *kappa, double *ebar);
+void orc_risk_score(int n_units, const int32_t *unit_class, int n_classes, const double *kappa,
+                    const double *ebar, const float *exposure, double *psi);
+
+/* ---- structural sparsity of the update coefficients (App. D.3, diagnostic
+ *      replays).  coeff f64 [R*T], flags u8 [R*T] (bit 1 = clipped), adv f32 [R],
+ *      mask u8 [R*T] or NULL.  counts[3] = padding, zero-advantage, clipped slots;
+ *      returns the top-k share of sum |omega|. */
+double orc_update_sparsity(const double *coeff, const uint8_t *flags, const float *adv,
+                           const uint8_t *mask, int R, int T, double top_frac, int64_t *counts);
+
 #ifdef __cplusplus
 }
 #endif
