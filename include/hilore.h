@@ -11,6 +11,11 @@
  *   Allocate        joint H/L/R choice under memory and risk -> hilore_allocate
  *   in backward     reconstruct L units                     -> hilore_decompress
  *                   and consume them in the weight gradient -> hilore_dequant_wgrad
+ * Calibration (App. B.1), before training and between refreshes:
+ *   single-unit gradient error y                             -> hilore_grad_rel_err
+ *   susceptibility kappa_c and mean reconstruction error     -> hilore_calibrate
+ *   psi_u = kappa E_u ebar_u, the risk input of Allocate     -> hilore_risk_score
+ * Diagnostics (App. D.3): zero-gradient causes, top-k share  -> hilore_update_sparsity
  *
  * Conventions shared by every entry point:
  *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The
@@ -247,6 +252,82 @@ hilore_status hilore_allocate(int n_units, const uint8_t *q, const uint8_t *veri
                               double delta_b, int n_b, int n_d, uint8_t *action, double *totals,
                               int64_t *jk, void *workspace, size_t workspace_bytes,
                               void *stream);
+
+/*
+ * Relative gradient error of one single-unit L intervention, the calibration
+ * target y of App. B.1 Eq. app-calibration-error (Sec. 3.4 Eq.
+ * calibration-metrics):
+ *   y = sqrt( ||g_l - g_ex||^2 / max(||g_ex||^2, eps_num) )    (the paper: eps_num = 1e-30)
+ *   g_l, g_ex  f32 [n]: the trainable-parameter gradients with unit u in L and with
+ *              exact recovery, e.g. two outputs of hilore_dequant_wgrad (16-byte aligned)
+ *   y          f32 [1] (device, 4-byte aligned; may point into the grad_err array of
+ *              hilore_calibrate)
+ * The sums are fp64 over the fp32 values, in a fixed order (per-workgroup partial
+ * sums in `workspace`, then one fixed tree).  workspace: device memory of at least
+ * hilore_grad_rel_err_workspace_bytes(n) bytes (at most 16 KB), 16-byte aligned;
+ * its contents on entry do not matter; calls sharing it must not overlap.
+ * n = 0 gives y = 0.  Errors: n < 0, eps_num not positive and finite, null
+ * pointers -> INVALID_ARG; workspace too small -> WORKSPACE.
+ */
+size_t hilore_grad_rel_err_workspace_bytes(int64_t n);
+hilore_status hilore_grad_rel_err(const float *g_l, const float *g_ex, int64_t n, double eps_num,
+                                  float *y, void *workspace, size_t workspace_bytes,
+                                  void *stream);
+
+/*
+ * Calibration of the L risk (App. B.1 Eqs. app-kappa and app-risk-score; Sec.
+ * 3.4 Eq. susceptibility), from n_batches calibration microbatches.  Row b of
+ * each [n_batches][n_units] f32 array holds, per unit, the exposure E (from
+ * hilore_unit_exposure_risk), the reconstruction error e^L (its rel_err output)
+ * and the measured gradient error y (hilore_grad_rel_err).  unit_class i32
+ * [n_units] gives the class c(u) (saved-state type and layer); units outside
+ * [0, n_classes) take no part in any fit.  Outputs (device):
+ *   kappa f64 [n_classes]  kappa_c = max(0, sum x y / sum x^2) over the pairs (u, b)
+ *                          of class c, x = E e^L: the least-squares fit of y = kappa x
+ *                          over kappa >= 0 (0 when sum x^2 = 0)
+ *   ebar  f64 [n_units]    mean over b of e^L (0 when n_batches = 0), summed in
+ *                          batch order
+ * fp64 arithmetic; kappa's sums run in a fixed order.  Errors: negative sizes,
+ * null pointers -> INVALID_ARG; n_units * n_batches >= 2^31 -> UNSUPPORTED.
+ */
+hilore_status hilore_calibrate(int n_units, int n_batches, int n_classes,
+                               const int32_t *unit_class, const float *exposure,
+                               const float *rel_err, const float *grad_err, double *kappa,
+                               double *ebar, void *stream);
+
+/*
+ * Calibrated risk of each unit's L action for the current microbatch (App. B.1
+ * Eq. app-risk-score, equal to Sec. 3.4 Eq. token-weighted-risk):
+ *   psi[u] = kappa[c(u)] * exposure[u] * ebar[u]   (fp64, multiplied in that order)
+ * exposure f32 [n_units] from hilore_unit_exposure_risk; kappa, ebar from
+ * hilore_calibrate.  A unit whose class is outside [0, n_classes) has psi = +inf,
+ * which makes L unavailable in hilore_allocate (psi is its risk input).
+ * Errors: negative sizes, null pointers -> INVALID_ARG.
+ */
+hilore_status hilore_risk_score(int n_units, const int32_t *unit_class, int n_classes,
+                                const double *kappa, const double *ebar, const float *exposure,
+                                double *psi, void *stream);
+
+/*
+ * Structural sparsity of one batch of update coefficients (the diagnostic
+ * statistics of App. D.3), over the n = R*T response slots, padding included.
+ *   coeff f32 [R*T], flags u8 [R*T], adv f32 [R]: outputs of hilore_grpo_coeffs;
+ *   mask u8 [R*T] or NULL (all valid), as passed to it
+ * Outputs (device):
+ *   counts i64 [3]  slots whose policy gradient is zero, by exclusive cause:
+ *                   [0] padding (mask 0), [1] valid slots of a zero-advantage
+ *                   response, [2] valid nonzero-advantage slots on the flat clipped
+ *                   branch (flag bit 1); divide by n for the fractions
+ *   top_share f64 [1]  share of sum |omega| held by the k = max(1, ceil(top_frac * n))
+ *                   largest |omega| (padding counts as 0); 0 when every omega is 0
+ * The k-th largest |omega| is found exactly (radix select on the fp32 bit patterns)
+ * and ties do not change the result; the sums are fp64 in a fixed order.
+ * One workgroup (a diagnostic, not a hot-path step).  Errors: negative sizes,
+ * top_frac outside (0, 1], null pointers -> INVALID_ARG; R*T >= 2^31 -> UNSUPPORTED.
+ */
+hilore_status hilore_update_sparsity(const float *coeff, const uint8_t *flags, const float *adv,
+                                     const uint8_t *mask, int R, int T, double top_frac,
+                                     int64_t *counts, double *top_share, void *stream);
 
 #ifdef __cplusplus
 }

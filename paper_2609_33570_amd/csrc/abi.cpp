@@ -332,4 +332,93 @@ hilore_status hilore_allocate(int n_units, const uint8_t *q, const uint8_t *veri
   return hip_status(hilore::launch_allocate(a, KB, KD, workspace, static_cast<hipStream_t>(stream)));
 }
 
+size_t hilore_grad_rel_err_workspace_bytes(int64_t n) {
+  if (n < 0) return 0;
+  return (size_t)hilore::rel_err_partials(n) * 2 * sizeof(double);
+}
+
+hilore_status hilore_grad_rel_err(const float *g_l, const float *g_ex, int64_t n, double eps_num,
+                                  float *y, void *workspace, size_t workspace_bytes,
+                                  void *stream) {
+  if (n < 0 || !(eps_num > 0.0) || !std::isfinite(eps_num)) return HILORE_ERR_INVALID_ARG;
+  if (!y || !workspace || (n > 0 && (!g_l || !g_ex))) return HILORE_ERR_INVALID_ARG;
+  if ((n > 0 && (!aligned16(g_l) || !aligned16(g_ex))) || !aligned16(workspace) ||
+      (reinterpret_cast<uintptr_t>(y) & 3u) != 0)
+    return HILORE_ERR_ALIGNMENT;
+  if (workspace_bytes < hilore_grad_rel_err_workspace_bytes(n)) return HILORE_ERR_WORKSPACE;
+  return hip_status(hilore::launch_grad_rel_err(g_l, g_ex, n, eps_num, y,
+                                                static_cast<double *>(workspace),
+                                                static_cast<hipStream_t>(stream)));
+}
+
+hilore_status hilore_calibrate(int n_units, int n_batches, int n_classes,
+                               const int32_t *unit_class, const float *exposure,
+                               const float *rel_err, const float *grad_err, double *kappa,
+                               double *ebar, void *stream) {
+  if (n_units < 0 || n_batches < 0 || n_classes < 0) return HILORE_ERR_INVALID_ARG;
+  if ((int64_t)n_units * n_batches >= (int64_t(1) << 31)) return HILORE_ERR_UNSUPPORTED;
+  if ((n_classes > 0 && !kappa) || (n_units > 0 && (!unit_class || !ebar)) ||
+      ((int64_t)n_units * n_batches > 0 && (!exposure || !rel_err || !grad_err)))
+    return HILORE_ERR_INVALID_ARG;
+  const void *f32[] = {unit_class, exposure, rel_err, grad_err};
+  for (const void *p : f32)
+    if ((reinterpret_cast<uintptr_t>(p) & 3u) != 0) return HILORE_ERR_ALIGNMENT;
+  if ((reinterpret_cast<uintptr_t>(kappa) & 7u) != 0 || (reinterpret_cast<uintptr_t>(ebar) & 7u) != 0)
+    return HILORE_ERR_ALIGNMENT;
+  hilore::CalibArgs a{};
+  a.n_units = n_units;
+  a.n_batches = n_batches;
+  a.n_classes = n_classes;
+  a.unit_class = unit_class;
+  a.exposure = exposure;
+  a.rel_err = rel_err;
+  a.grad_err = grad_err;
+  a.kappa = kappa;
+  a.ebar = ebar;
+  return hip_status(hilore::launch_calibrate(a, static_cast<hipStream_t>(stream)));
+}
+
+hilore_status hilore_risk_score(int n_units, const int32_t *unit_class, int n_classes,
+                                const double *kappa, const double *ebar, const float *exposure,
+                                double *psi, void *stream) {
+  if (n_units < 0 || n_classes < 0) return HILORE_ERR_INVALID_ARG;
+  if (n_units == 0) return HILORE_OK;
+  if (!unit_class || !ebar || !exposure || !psi || (n_classes > 0 && !kappa))
+    return HILORE_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(unit_class) & 3u) != 0 ||
+      (reinterpret_cast<uintptr_t>(exposure) & 3u) != 0 ||
+      (reinterpret_cast<uintptr_t>(kappa) & 7u) != 0 ||
+      (reinterpret_cast<uintptr_t>(ebar) & 7u) != 0 || (reinterpret_cast<uintptr_t>(psi) & 7u) != 0)
+    return HILORE_ERR_ALIGNMENT;
+  return hip_status(hilore::launch_risk_score(n_units, unit_class, n_classes, kappa, ebar,
+                                              exposure, psi, static_cast<hipStream_t>(stream)));
+}
+
+hilore_status hilore_update_sparsity(const float *coeff, const uint8_t *flags, const float *adv,
+                                     const uint8_t *mask, int R, int T, double top_frac,
+                                     int64_t *counts, double *top_share, void *stream) {
+  if (R < 0 || T < 0 || !(top_frac > 0.0 && top_frac <= 1.0)) return HILORE_ERR_INVALID_ARG;
+  const int64_t n = (int64_t)R * T;
+  if (n >= (int64_t(1) << 31)) return HILORE_ERR_UNSUPPORTED;
+  if (!counts || !top_share || (n > 0 && (!coeff || !flags || !adv))) return HILORE_ERR_INVALID_ARG;
+  if ((reinterpret_cast<uintptr_t>(coeff) & 3u) != 0 || (reinterpret_cast<uintptr_t>(adv) & 3u) != 0 ||
+      (reinterpret_cast<uintptr_t>(counts) & 7u) != 0 ||
+      (reinterpret_cast<uintptr_t>(top_share) & 7u) != 0)
+    return HILORE_ERR_ALIGNMENT;
+  long long k = (long long)std::ceil(top_frac * (double)n);
+  if (k < 1) k = 1;
+  if (k > n) k = n;
+  hilore::SparsityArgs a{};
+  a.coeff = coeff;
+  a.flags = flags;
+  a.adv = adv;
+  a.mask = mask;
+  a.R = R;
+  a.T = T;
+  a.k = k;
+  a.counts = counts;
+  a.share = top_share;
+  return hip_status(hilore::launch_sparsity(a, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

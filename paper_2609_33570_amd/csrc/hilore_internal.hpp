@@ -124,4 +124,34 @@ constexpr int kAllocMaxUnits = 1 << 20;
 AllocLayout alloc_layout(int U, int KB, int KD);
 hipError_t launch_allocate(const AllocArgs &a, int KB, int KD, void *workspace, hipStream_t s);
 
+// Calibration scalars (App. B.1 Eqs. app-calibration-error, app-kappa,
+// app-risk-score) and the update-sparsity diagnostics (App. D.3).
+constexpr int kRelMaxPartials = 1024;  // workgroups of the relative-error reduction
+int rel_err_partials(int64_t n);       // how many of them a reduction over n uses
+hipError_t launch_grad_rel_err(const float *g_l, const float *g_ex, int64_t n, double eps_num,
+                               float *y, double *part, hipStream_t s);
+
+struct CalibArgs {
+  int n_units, n_batches, n_classes;
+  const int32_t *unit_class;
+  const float *exposure, *rel_err, *grad_err;  // [n_batches][n_units]
+  double *kappa, *ebar;
+};
+hipError_t launch_calibrate(const CalibArgs &a, hipStream_t s);
+hipError_t launch_risk_score(int n_units, const int32_t *unit_class, int n_classes,
+                             const double *kappa, const double *ebar, const float *exposure,
+                             double *psi, hipStream_t s);
+
+struct SparsityArgs {
+  const float *coeff;
+  const uint8_t *flags;
+  const float *adv;
+  const uint8_t *mask;
+  int R, T;
+  long long k;  // ranks in the top share, 1 <= k <= R*T
+  int64_t *counts;
+  double *share;
+};
+hipError_t launch_sparsity(const SparsityArgs &a, hipStream_t s);
+
 }  // namespace hilore

@@ -77,6 +77,11 @@ def load() -> ctypes.CDLL:
         "hilore_allocate_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32]),
         "hilore_allocate": (i32, [i32, P, P, P, P, P, P, P, f64, f64, i32, i32, P, P, P, P,
                                   ctypes.c_size_t, P]),
+        "hilore_grad_rel_err_workspace_bytes": (ctypes.c_size_t, [i64]),
+        "hilore_grad_rel_err": (i32, [P, P, i64, f64, P, P, ctypes.c_size_t, P]),
+        "hilore_calibrate": (i32, [i32, i32, i32, P, P, P, P, P, P, P]),
+        "hilore_risk_score": (i32, [i32, P, i32, P, P, P, P, P]),
+        "hilore_update_sparsity": (i32, [P, P, P, P, i32, i32, f64, P, P, P]),
     }
     for name, (res, args) in sig.items():
         fn = getattr(L, name)
@@ -202,3 +207,42 @@ def hilore_allocate(q, verified, tau_h, tau_l, dm_h, dm_l, psi, m_res: float, de
                                   _p(dm_l), _p(psi), float(m_res), float(delta_b), int(n_b),
                                   int(n_d), _p(action), _p(totals), _p(jk), _p(workspace),
                                   ws_bytes, _stream(stream)))
+
+
+def hilore_grad_rel_err_workspace_bytes(n: int) -> int:
+    return int(load().hilore_grad_rel_err_workspace_bytes(int(n)))
+
+
+def hilore_grad_rel_err(g_l, g_ex, y, workspace, eps_num: float = 1e-30, stream=None):
+    """y (a one-element f32 device tensor or view) = relative gradient error of
+    g_l against g_ex (f32 device tensors of equal size)."""
+    n = int(g_ex.numel())
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("hilore_grad_rel_err",
+           load().hilore_grad_rel_err(_p(g_l), _p(g_ex), n, float(eps_num), _p(y), _p(workspace),
+                                      ws_bytes, _stream(stream)))
+
+
+def hilore_calibrate(unit_class, exposure, rel_err, grad_err, n_classes: int, kappa, ebar,
+                     stream=None):
+    """exposure, rel_err, grad_err: f32 device tensors [n_batches, n_units];
+    unit_class i32 [n_units]; kappa f64 [n_classes], ebar f64 [n_units]."""
+    nb, nu = (int(d) for d in exposure.shape)
+    _check("hilore_calibrate",
+           load().hilore_calibrate(nu, nb, int(n_classes), _p(unit_class), _p(exposure),
+                                   _p(rel_err), _p(grad_err), _p(kappa), _p(ebar),
+                                   _stream(stream)))
+
+
+def hilore_risk_score(unit_class, kappa, ebar, exposure, psi, stream=None):
+    _check("hilore_risk_score",
+           load().hilore_risk_score(int(unit_class.numel()), _p(unit_class), int(kappa.numel()),
+                                    _p(kappa), _p(ebar), _p(exposure), _p(psi), _stream(stream)))
+
+
+def hilore_update_sparsity(coeff, flags, adv, mask, R: int, T: int, top_frac: float, counts,
+                           top_share, stream=None):
+    _check("hilore_update_sparsity",
+           load().hilore_update_sparsity(_p(coeff), _p(flags), _p(adv), _p(mask), int(R), int(T),
+                                         float(top_frac), _p(counts), _p(top_share),
+                                         _stream(stream)))

@@ -218,3 +218,46 @@ def test_allocate_validation(lib):
         E.HILORE_ERR_INVALID_ARG
     # zero budgets leave a single state per axis: a small workspace is checked too
     assert alloc(lib, m_res=0.0, delta_b=0.0, ws_bytes=1000) == E.HILORE_ERR_WORKSPACE
+
+
+def test_calibration_entry_points_validate(lib):
+    E = hilore
+    big = 1 << 20
+    ws = lib.hilore_grad_rel_err_workspace_bytes
+    assert ws(0) == 16 and ws(1 << 24) == 16 * 1024 and ws(1 << 30) == 16 * 1024 and ws(-1) == 0
+    rel = lib.hilore_grad_rel_err
+    assert rel(FAKE, FAKE, 1000, 1e-30, FAKE, FAKE, 15, None) == E.HILORE_ERR_WORKSPACE
+    assert rel(FAKE, FAKE, -1, 1e-30, FAKE, FAKE, big, None) == E.HILORE_ERR_INVALID_ARG
+    assert rel(FAKE, FAKE, 10, 0.0, FAKE, FAKE, big, None) == E.HILORE_ERR_INVALID_ARG
+    assert rel(FAKE, FAKE, 10, float("inf"), FAKE, FAKE, big, None) == E.HILORE_ERR_INVALID_ARG
+    assert rel(None, FAKE, 10, 1e-30, FAKE, FAKE, big, None) == E.HILORE_ERR_INVALID_ARG
+    assert rel(FAKE, FAKE, 10, 1e-30, None, FAKE, big, None) == E.HILORE_ERR_INVALID_ARG
+    assert rel(FAKE + 4, FAKE, 10, 1e-30, FAKE, FAKE, big, None) == E.HILORE_ERR_ALIGNMENT
+    assert rel(FAKE, FAKE, 10, 1e-30, FAKE + 2, FAKE, big, None) == E.HILORE_ERR_ALIGNMENT
+    assert rel(FAKE, FAKE, 10, 1e-30, FAKE, FAKE + 8, big, None) == E.HILORE_ERR_ALIGNMENT
+
+    cal = lib.hilore_calibrate
+    assert cal(-1, 2, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert cal(4, 2, -1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert cal(1 << 16, 1 << 15, 1, FAKE, FAKE, FAKE, FAKE, FAKE, FAKE, None) == \
+        E.HILORE_ERR_UNSUPPORTED
+    assert cal(4, 2, 1, FAKE, None, FAKE, FAKE, FAKE, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert cal(4, 2, 1, FAKE, FAKE, FAKE, FAKE, None, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert cal(4, 2, 1, FAKE, FAKE, FAKE + 2, FAKE, FAKE, FAKE, None) == E.HILORE_ERR_ALIGNMENT
+    assert cal(4, 2, 1, FAKE, FAKE, FAKE, FAKE, FAKE + 4, FAKE, None) == E.HILORE_ERR_ALIGNMENT
+
+    risk = lib.hilore_risk_score
+    assert risk(-1, FAKE, 1, FAKE, FAKE, FAKE, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert risk(4, FAKE, 1, FAKE, FAKE, FAKE, None, None) == E.HILORE_ERR_INVALID_ARG
+    assert risk(4, FAKE, 1, FAKE, FAKE, FAKE, FAKE + 4, None) == E.HILORE_ERR_ALIGNMENT
+    assert risk(0, None, 0, None, None, None, None, None) == E.HILORE_OK
+
+    sp = lib.hilore_update_sparsity
+    assert sp(FAKE, FAKE, FAKE, None, 4, 8, 0.0, FAKE, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert sp(FAKE, FAKE, FAKE, None, 4, 8, 1.5, FAKE, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert sp(FAKE, FAKE, FAKE, None, -4, 8, 0.1, FAKE, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert sp(FAKE, FAKE, FAKE, None, 1 << 16, 1 << 15, 0.1, FAKE, FAKE, None) == \
+        E.HILORE_ERR_UNSUPPORTED
+    assert sp(FAKE, None, FAKE, None, 4, 8, 0.1, FAKE, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert sp(FAKE, FAKE, FAKE, None, 4, 8, 0.1, None, FAKE, None) == E.HILORE_ERR_INVALID_ARG
+    assert sp(FAKE, FAKE, FAKE, None, 4, 8, 0.1, FAKE + 4, FAKE, None) == E.HILORE_ERR_ALIGNMENT
