@@ -318,3 +318,12 @@ def update_sparsity(coeff, flags, adv, mask, R, T, top_frac=0.1):
     share = lib().orc_update_sparsity(_ptr(w), _ptr(f), _ptr(a), None if m is None else _ptr(m.ravel()),
                                       int(R), int(T), float(top_frac), _ptr(counts))
     return counts, share
+
+
+def lora_down_grad(codes, scales, code, block, dh_u16, scale=1.0, variant=0):
+    """Gradient of the LoRA down-projection weight A [r, in] of a linear layer
+    whose saved input X [K, in] is an L unit: with h = X A^T, z = h B^T and
+    the layer output y = X W^T + scale * z (PEFT's convention, scale = alpha/r),
+    dA = scale * (G B)^T X = scale * dh^T X with dh = G B [K, r].  This is the
+    weight gradient X^T dh of orc_wgrad, transposed and scaled."""
+    return scale * wgrad(codes, scales, code, block, dh_u16, variant=variant).T
