@@ -11,6 +11,7 @@
  *   Allocate        joint H/L/R choice under memory and risk -> hilore_allocate
  *   in backward     reconstruct L units                     -> hilore_decompress
  *                   and consume them in the weight gradient -> hilore_dequant_wgrad
+ *                   or in the LoRA adapter gradient          -> hilore_dequant_lora_grad
  * Calibration (App. B.1), before training and between refreshes:
  *   single-unit gradient error y                             -> hilore_grad_rel_err
  *   susceptibility kappa_c and mean reconstruction error     -> hilore_calibrate
@@ -208,6 +209,36 @@ hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask,
 hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, int code,
                                    int block, const uint16_t *dy, float *dw, int64_t K,
                                    int64_t M, int64_t N, int accumulate, void *stream);
+
+/*
+ * Gradient of the LoRA down-projection A of a linear layer whose saved input X
+ * is an L unit, with the reconstruction fused into the operand load (the
+ * paper's default training setting: rank-16 adapters, alpha = 32, on q/k/v/o
+ * and gate/up/down, only adapters trainable, App. D.1.1).  With the layer
+ * output y = X W^T + scale * (X A^T) B^T and an upstream gradient G, and
+ * dh = G B (the gradient of h = X A^T before the scaling):
+ *   dA[j][i] (+)= scale * sum_t dh[t][j] * xhat[t][i],
+ *   xhat = bf16_RNE(value(code[t][i]) * scale[t][i/block])   (the hilore_decompress value)
+ *   x_codes  [K, M] one byte per element; x_scales f32 [K, M / block]
+ *   dh       bf16 [K, r] row-major; da f32 [r, M] row-major (the layout of A's gradient)
+ *   scale    the adapter scaling alpha / r (applied to the fp32 sum; exact for powers of 2)
+ *   accumulate: 0 overwrites da, 1 adds to it
+ * bf16 x bf16 products, fp32 accumulation (MFMA), xhat never written to memory;
+ * each code is read once per 16 adapter rows.  Partial sums over token ranges
+ * go to `workspace` and are added in a fixed order (no floating-point atomics).
+ * workspace: device memory of at least hilore_lora_grad_workspace_bytes(K, M, r)
+ * bytes (8 MB below M = 65536 columns), 16-byte aligned,
+ * contents on entry irrelevant; calls sharing it must not overlap.
+ * With HILORE_CODE_FP8_E4M3FN_CAST (block = 0, x_scales unused) xhat = value(code).
+ * Limits: M % block == 0, M % 16 == 0, M < 2^26, K < 2^31, r even, 2 <= r <= 4096.
+ * Errors: negative sizes, r < 1, non-finite scale, null pointers -> INVALID_ARG;
+ * other shapes (odd r included) -> UNSUPPORTED; workspace too small -> WORKSPACE.
+ */
+size_t hilore_lora_grad_workspace_bytes(int64_t K, int64_t M, int r);
+hilore_status hilore_dequant_lora_grad(const void *x_codes, const float *x_scales, int code,
+                                       int block, const uint16_t *dh, float *da, int64_t K,
+                                       int64_t M, int r, float scale, int accumulate,
+                                       void *workspace, size_t workspace_bytes, void *stream);
 
 /*
  * Joint H/L/R recovery allocation of one microbatch (Sec. 3.4 Eq.

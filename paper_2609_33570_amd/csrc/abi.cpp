@@ -421,4 +421,47 @@ hilore_status hilore_update_sparsity(const float *coeff, const uint8_t *flags, c
   return hip_status(hilore::launch_sparsity(a, static_cast<hipStream_t>(stream)));
 }
 
+size_t hilore_lora_grad_workspace_bytes(int64_t K, int64_t M, int r) {
+  if (K < 0 || M < 0 || r < 1) return 0;
+  return hilore::lora_plan(K, M, r).workspace_bytes;
+}
+
+hilore_status hilore_dequant_lora_grad(const void *x_codes, const float *x_scales, int code,
+                                       int block, const uint16_t *dh, float *da, int64_t K,
+                                       int64_t M, int r, float scale, int accumulate,
+                                       void *workspace, size_t workspace_bytes, void *stream) {
+  if (K < 0 || M < 0 || r < 1 || !std::isfinite(scale)) return HILORE_ERR_INVALID_ARG;
+  const hilore_status cb = check_code_block(code, block);
+  if (cb != HILORE_OK) return cb;
+  const bool cast = code == HILORE_CODE_FP8_E4M3FN_CAST;
+  if ((!cast && M % block != 0) || M % 16 != 0 || r % 2 != 0 || r > 4096)
+    return HILORE_ERR_UNSUPPORTED;
+  if (M >= (int64_t(1) << 26) || K >= (int64_t(1) << 31)) return HILORE_ERR_UNSUPPORTED;
+  if (M == 0) return HILORE_OK;
+  if (!da || !workspace) return HILORE_ERR_INVALID_ARG;
+  if (K > 0 && (!x_codes || (!cast && !x_scales) || !dh)) return HILORE_ERR_INVALID_ARG;
+  const void *ptrs[] = {x_codes, x_scales, dh, da, workspace};
+  for (const void *p : ptrs)
+    if (p && !aligned16(p)) return HILORE_ERR_ALIGNMENT;
+  const hilore::LoraPlan plan = hilore::lora_plan(K, M, r);
+  if (workspace_bytes < plan.workspace_bytes) return HILORE_ERR_WORKSPACE;
+  hilore::LoraArgs a{};
+  a.codes = static_cast<const uint8_t *>(x_codes);
+  a.scales = cast ? nullptr : x_scales;
+  a.dh = dh;
+  a.da = da;
+  a.part = static_cast<float *>(workspace);
+  a.K = K;
+  a.M = M;
+  a.ldh = r;
+  a.scale = scale;
+  a.accumulate = accumulate ? 1 : 0;
+  a.S = plan.S;
+  a.KS = plan.KS;
+  a.U = plan.U;
+  a.n_wg = plan.n_wg;
+  a.xcd_remap = plan.xcd_remap;
+  return hip_status(hilore::launch_lora(a, code, block, r, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

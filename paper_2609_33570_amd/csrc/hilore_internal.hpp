@@ -154,4 +154,29 @@ struct SparsityArgs {
 };
 hipError_t launch_sparsity(const SparsityArgs &a, hipStream_t s);
 
+// LoRA adapter gradient on an L unit (App. D.1.1 adapters; App. B.1 codec).
+constexpr int kLoraWorkgroups = 256;  // stream-K grid: one workgroup per CU
+struct LoraPlan {
+  int64_t S, KS, U;  // strips of 256 columns, k-steps of 32 rows per strip, S * KS
+  int64_t n_wg;      // workgroups of the main kernel
+  int xcd_remap;     // give each XCD consecutive ranges
+  size_t workspace_bytes;
+  int passes;        // 16 adapter rows per pass
+};
+LoraPlan lora_plan(int64_t K, int64_t M, int r);
+struct LoraArgs {
+  const uint8_t *codes;
+  const float *scales;
+  const uint16_t *dh;  // bf16 [K, ldh]
+  float *da;           // f32 [r, M]
+  float *part;         // workspace: 2 partial [16][256] slots per workgroup
+  int64_t K, M;
+  int ldh, r0, r_pass;
+  float scale;
+  int accumulate;
+  int64_t S, KS, U, n_wg;
+  int xcd_remap;
+};
+hipError_t launch_lora(const LoraArgs &a, int code, int block, int r, hipStream_t s);
+
 }  // namespace hilore

@@ -77,6 +77,9 @@ def load() -> ctypes.CDLL:
         "hilore_allocate_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32]),
         "hilore_allocate": (i32, [i32, P, P, P, P, P, P, P, f64, f64, i32, i32, P, P, P, P,
                                   ctypes.c_size_t, P]),
+        "hilore_lora_grad_workspace_bytes": (ctypes.c_size_t, [i64, i64, i32]),
+        "hilore_dequant_lora_grad": (i32, [P, P, i32, i32, P, P, i64, i64, i32, f32, i32, P,
+                                           ctypes.c_size_t, P]),
         "hilore_grad_rel_err_workspace_bytes": (ctypes.c_size_t, [i64]),
         "hilore_grad_rel_err": (i32, [P, P, i64, f64, P, P, ctypes.c_size_t, P]),
         "hilore_calibrate": (i32, [i32, i32, i32, P, P, P, P, P, P, P]),
@@ -186,6 +189,23 @@ def hilore_dequant_wgrad(x_codes, x_scales, code, block: int, dy, dw, K: int, M:
            load().hilore_dequant_wgrad(_p(x_codes), _p(x_scales), _code(code), int(block),
                                        _p(dy), _p(dw), int(K), int(M), int(N),
                                        1 if accumulate else 0, _stream(stream)))
+
+
+def hilore_lora_grad_workspace_bytes(K: int, M: int, r: int) -> int:
+    return int(load().hilore_lora_grad_workspace_bytes(int(K), int(M), int(r)))
+
+
+def hilore_dequant_lora_grad(x_codes, x_scales, code, block: int, dh, da, K: int, M: int, r: int,
+                             scale: float, accumulate: bool, workspace, stream=None):
+    """dA [r, M] (+)= scale * dh^T xhat, xhat reconstructed from the codes in the
+    operand load; dh bf16 [K, r]; workspace a device tensor of at least
+    hilore_lora_grad_workspace_bytes(K, M, r) bytes."""
+    ws_bytes = workspace.numel() * workspace.element_size()
+    _check("hilore_dequant_lora_grad",
+           load().hilore_dequant_lora_grad(_p(x_codes), _p(x_scales), _code(code), int(block),
+                                           _p(dh), _p(da), int(K), int(M), int(r), float(scale),
+                                           1 if accumulate else 0, _p(workspace), ws_bytes,
+                                           _stream(stream)))
 
 
 ACT_R, ACT_H, ACT_L = 0, 1, 2

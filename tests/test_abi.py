@@ -261,3 +261,37 @@ def test_calibration_entry_points_validate(lib):
     assert sp(FAKE, None, FAKE, None, 4, 8, 0.1, FAKE, FAKE, None) == E.HILORE_ERR_INVALID_ARG
     assert sp(FAKE, FAKE, FAKE, None, 4, 8, 0.1, None, FAKE, None) == E.HILORE_ERR_INVALID_ARG
     assert sp(FAKE, FAKE, FAKE, None, 4, 8, 0.1, FAKE + 4, FAKE, None) == E.HILORE_ERR_ALIGNMENT
+
+
+def test_lora_grad_validation(lib):
+    E = hilore
+    ws = lib.hilore_lora_grad_workspace_bytes
+    # 256 workgroups x 2 partial [16][256] fp32 slots (a range meets at most two strips)
+    assert ws(16384, 18944, 16) == 256 * 2 * 16 * 256 * 4
+    assert ws(16384, 18944, 64) == ws(16384, 18944, 16)  # passes reuse the slots
+    assert ws(32, 256, 16) == 1 * 2 * 16 * 256 * 4       # one k-step: one workgroup
+    assert ws(-1, 256, 16) == 0 and ws(32, 256, 0) == 0
+    big = 1 << 30
+
+    def call(**kw):
+        a = dict(codes=FAKE, scales=FAKE, code=1, block=128, dh=FAKE, da=FAKE, K=1024, M=1024,
+                 r=16, scale=2.0, acc=0, ws=FAKE, ws_bytes=big)
+        a.update(kw)
+        return lib.hilore_dequant_lora_grad(a["codes"], a["scales"], a["code"], a["block"],
+                                            a["dh"], a["da"], a["K"], a["M"], a["r"], a["scale"],
+                                            a["acc"], a["ws"], a["ws_bytes"], None)
+    assert call(ws_bytes=ws(1024, 1024, 16) - 1) == E.HILORE_ERR_WORKSPACE
+    assert call(K=-1) == E.HILORE_ERR_INVALID_ARG
+    assert call(r=0) == E.HILORE_ERR_INVALID_ARG
+    assert call(scale=float("nan")) == E.HILORE_ERR_INVALID_ARG
+    assert call(code=7) == E.HILORE_ERR_INVALID_ARG
+    assert call(block=48) == E.HILORE_ERR_UNSUPPORTED
+    assert call(M=1000) == E.HILORE_ERR_UNSUPPORTED            # not a block multiple
+    assert call(code=2, block=0, M=1000) == E.HILORE_ERR_UNSUPPORTED  # not a multiple of 16
+    assert call(r=4098) == E.HILORE_ERR_UNSUPPORTED
+    assert call(r=17) == E.HILORE_ERR_UNSUPPORTED  # odd ranks: dh rows are read in pairs
+    for name in ("codes", "scales", "dh", "da", "ws"):
+        assert call(**{name: None}) == E.HILORE_ERR_INVALID_ARG, name
+    for name in ("codes", "scales", "dh", "da", "ws"):
+        assert call(**{name: FAKE + 8}) == E.HILORE_ERR_ALIGNMENT, name
+    assert call(M=0, da=None) == E.HILORE_OK  # nothing to do
