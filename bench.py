@@ -18,7 +18,9 @@ Prints ONE JSON line.  `value` is compress+decompress throughput in GB/s of
 algorithmic bytes (the first figure of the metric); the wgrad TFLOP/s and the
 coefficient tokens/s ride along, each with its own roofline.  For context the
 line also times hilore_allocate (the H/L/R dynamic programme that follows the
-exposure step) on a 196-unit plan, outside the step.
+exposure step) on a 196-unit plan, and, under "next", the calls that follow
+the five rows (the LoRA adapter gradient on the MLP unit, the calibration
+scalars, the update-sparsity diagnostics), all outside the step.
 """
 from __future__ import annotations
 
@@ -80,7 +82,8 @@ def measured_traffic():
     csrc = os.path.join(ROOT, "paper_2609_33570_amd", "csrc")
     common = ["device_common.hpp", "hilore_internal.hpp"]
     files = {"compress": ["codec.hip"], "decompress": ["codec.hip"], "dequant_wgrad": ["wgrad.hip"],
-             "grpo_coeffs": ["grpo.hip"], "exposure_risk": ["risk.hip"]}
+             "grpo_coeffs": ["grpo.hip"], "exposure_risk": ["risk.hip"],
+             "dequant_lora_grad": ["lora.hip"], "grad_rel_err": ["calib.hip"]}
     out = {}
     for k, ent in table.get("kernels", {}).items():
         h = hashlib.sha256()
@@ -276,6 +279,8 @@ def main():
 
     progress("timing the H/L/R allocation of a 196-unit plan")
     out["allocate"] = alloc_bench(hl, wl)
+    progress("timing the LoRA adapter gradient, calibration and diagnostics")
+    out["next"] = next_rows_bench(hl, wl, sets, w, code, block, rows, R)
     if args.blas_ref:
         progress("timing hipBLASLt on the reconstructed X")
         out["blas_ref"] = blas_ref(sets[0], code, block, K, M, N)
@@ -462,6 +467,99 @@ def alloc_bench(hl, wl, iters=10):
                        "L": int((a == 2).sum())}}
 
 
+def next_rows_bench(hl, wl, sets, w, code, block, rows, R, iters=20):
+    """Context, outside the step: the calls that follow the five hot-path rows,
+    on this microbatch's data.
+      lora_grad        hilore_dequant_lora_grad on the MLP unit's codes (16384 x 18944,
+                       rank 16): the adapter gradient of the paper's LoRA setting
+      grad_rel_err     hilore_grad_rel_err on two 4096 x 4096 fp32 gradients
+      calibrate        hilore_calibrate over 8 calibration microbatches x 196 units
+      risk_score       hilore_risk_score for 196 units
+      update_sparsity  hilore_update_sparsity on the 16384 coefficient slots
+    Each timed with HIP events on the stream it runs on, averaged over `iters`
+    calls that rotate over the buffer sets."""
+    import numpy as np
+    import torch
+
+    def timed(fn):
+        for i in range(3):
+            fn(i)
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        torch.cuda.synchronize()
+        e0.record()
+        for i in range(iters):
+            fn(i)
+        e1.record()
+        torch.cuda.synchronize()
+        return e0.elapsed_time(e1) / iters  # ms
+
+    def roof(name, nbytes, ms, per_unit):
+        a = nbytes / (ms * 1e-3) / 1e9
+        return {"kernel": name, "bound": "hbm", "achieved": round(a, 2), "peak": HBM_PEAK_GBS,
+                "unit": "GB/s", "frac": round(a / HBM_PEAK_GBS, 4), "us": round(ms * 1e3, 2),
+                "algorithmic": per_unit}
+
+    out = {}
+    # LoRA adapter gradient on the MLP unit of each set
+    u = w.units[1]
+    K, M, r = u.rows, u.cols, 16
+    dhs = [wl.normal_bf16_device(K, r, 500 + i, 0.05) for i in range(len(sets))]
+    da = torch.empty((r, M), dtype=torch.float32, device="cuda")
+    ws = torch.empty(hl.hilore_lora_grad_workspace_bytes(K, M, r), dtype=torch.uint8,
+                     device="cuda")
+
+    def lora(i):
+        st = sets[i % len(sets)]
+        _, codes, scales, _, _, _ = st["keep"][1]
+        hl.hilore_dequant_lora_grad(codes, scales, code, block, dhs[i % len(sets)], da, K, M, r,
+                                    2.0, False, ws)
+
+    ms = timed(lora)
+    lb = K * M + K * M * 4 // block + K * r * 2 + r * M * 4
+    out["lora_grad"] = roof("dequant_lora_grad", lb, ms,
+                            f"{lb} B per call: codes + scales of {K}x{M}, dh {K}x{r} bf16, "
+                            f"dA {r}x{M} fp32")
+    out["lora_grad"]["shape"] = {"K": K, "M": M, "r": r, "code": "fp8-e4m3fn", "block": block}
+    traffic = measured_traffic()
+    out["lora_grad"]["traffic"] = traffic.get("dequant_lora_grad")
+    # relative gradient error of two dW-sized fp32 gradients (the step's dW of two sets)
+    n = sets[0]["dw"].numel()
+    y = torch.empty(1, dtype=torch.float32, device="cuda")
+    wsr = torch.empty(hl.hilore_grad_rel_err_workspace_bytes(n), dtype=torch.uint8, device="cuda")
+
+    def rel(i):
+        hl.hilore_grad_rel_err(sets[i % len(sets)]["dw"], sets[(i + 1) % len(sets)]["dw"], y, wsr)
+
+    ms = timed(rel)
+    out["grad_rel_err"] = roof("grad_rel_err", 8 * n, ms, f"{8 * n} B per call (two fp32 [{n}])")
+    out["grad_rel_err"]["traffic"] = traffic.get("grad_rel_err")
+    # calibration scalars and risk scores: 196 units (28 layers x 7), 8 calibration microbatches
+    nu, nb, nc = 196, 8, 28 * 2
+    g = wl.rng(wl.BASE_SEED + 7, 1)
+    cls = torch.from_numpy((np.arange(nu) // 7 * 2 + (np.arange(nu) % 7 >= 4)).astype(np.int32)).cuda()
+    e = torch.from_numpy(g.uniform(0.1, 2.0, (nb, nu)).astype(np.float32)).cuda()
+    rl = torch.from_numpy(g.uniform(1e-3, 5e-2, (nb, nu)).astype(np.float32)).cuda()
+    yy = torch.from_numpy(g.uniform(0.0, 1e-2, (nb, nu)).astype(np.float32)).cuda()
+    kappa = torch.empty(nc, dtype=torch.float64, device="cuda")
+    ebar = torch.empty(nu, dtype=torch.float64, device="cuda")
+    psi = torch.empty(nu, dtype=torch.float64, device="cuda")
+    ms = timed(lambda i: hl.hilore_calibrate(cls, e, rl, yy, nc, kappa, ebar))
+    out["calibrate_us"] = round(ms * 1e3, 2)
+    ms = timed(lambda i: hl.hilore_risk_score(cls, kappa, ebar, e[0], psi))
+    out["risk_score_us"] = round(ms * 1e3, 2)
+    counts = torch.empty(3, dtype=torch.int64, device="cuda")
+    share = torch.empty(1, dtype=torch.float64, device="cuda")
+
+    def sparsity(i):
+        st = sets[i % len(sets)]
+        hl.hilore_update_sparsity(st["coeff"], st["flags"], st["adv"], None, R, rows // R, 0.1,
+                                  counts, share)
+
+    ms = timed(sparsity)
+    out["update_sparsity_us"] = round(ms * 1e3, 2)
+    return out
+
+
 def blas_ref(st, code, block, K, M, N, iters=10):
     """Context only: the library GEMM (torch.mm -> hipBLASLt, bf16 in, bf16
     out, fp32 accumulation) on X reconstructed by hilore_decompress, with X^T
@@ -533,6 +631,15 @@ def cpu_baseline(args, st, w, block, code):
     t0 = time.perf_counter()
     oracle.allocate(*inst.arrays(), inst.m_res, inst.delta_b, n_b=1024, n_d=1024)
     dt_alloc = time.perf_counter() - t0
+    # LoRA adapter gradient (rank 16) on the first 256 columns of the MLP unit
+    _, mc, msc, _, _, _ = st["keep"][1]
+    lc = mc[:, :256].cpu().contiguous().numpy()
+    lsc = msc[:, :256 // block].cpu().contiguous().numpy()
+    dh = wl.normal_bf16_host(lc.shape[0], 16, seed=wl.BASE_SEED + 9, sigma=0.05)
+    t0 = time.perf_counter()
+    oracle.lora_down_grad(lc, lsc, code, block, dh, scale=2.0, variant=0)
+    dt_lora = time.perf_counter() - t0
+    lora_bytes = lc.size + lsc.size * 4 + dh.size * 2 + 16 * 256 * 4
     return {
         "value": round(total / dt_codec / 1e9, 4),
         "unit": "GB/s",
@@ -546,6 +653,8 @@ def cpu_baseline(args, st, w, block, code):
         "wgrad_sample": f"dW[0:128, 0:128] over K={K} in fp64, {dt_w:.1f} s",
         "allocate_ms": round(dt_alloc * 1e3, 1),
         "allocate_sample": "the same 196-unit plan on the 1025 x 1025 grid",
+        "lora_grad_gbs": round(lora_bytes / dt_lora / 1e9, 4),
+        "lora_grad_sample": f"rank-16 dA over {lc.shape[0]}x256 MLP codes in fp64, {dt_lora:.1f} s",
     }
 
 
