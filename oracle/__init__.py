@@ -78,6 +78,7 @@ def lib() -> ctypes.CDLL:
             "orc_calibrate": (None, [i32, i32, i32, P, P, P, P, P, P]),
             "orc_risk_score": (None, [i32, P, i32, P, P, P, P]),
             "orc_update_sparsity": (f64, [P, P, P, P, i32, i32, f64, P]),
+            "orc_swiglu_bwd": (None, [P, P, P, i64, P, P]),
         }
         for name, (res, args) in sig.items():
             fn = getattr(L, name)
@@ -327,3 +328,15 @@ def lora_down_grad(codes, scales, code, block, dh_u16, scale=1.0, variant=0):
     dA = scale * (G B)^T X = scale * dh^T X with dh = G B [K, r].  This is the
     weight gradient X^T dh of orc_wgrad, transposed and scaled."""
     return scale * wgrad(codes, scales, code, block, dh_u16, variant=variant).T
+
+
+def swiglu_bwd(g, u, dh):
+    """Backward of h = silu(g) * u in fp64: returns (dg, du) with the shape of g."""
+    g64 = _c(g, np.float64)
+    u64 = _c(u, np.float64)
+    d64 = _c(dh, np.float64)
+    assert g64.shape == u64.shape == d64.shape
+    dg = np.empty(g64.shape, dtype=np.float64)
+    du = np.empty(g64.shape, dtype=np.float64)
+    lib().orc_swiglu_bwd(_ptr(g64), _ptr(u64), _ptr(d64), g64.size, _ptr(dg), _ptr(du))
+    return dg, du

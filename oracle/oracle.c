@@ -746,3 +746,22 @@ double orc_update_sparsity(const double *coeff, const uint8_t *flags, const floa
   free(mag);
   return share;
 }
+
+/* ======================================================================= */
+/* Backward of the gated MLP activation on a reconstructed unit            */
+/* ======================================================================= */
+
+/* The gated MLP of the evaluated models computes h = silu(g) * u from the
+ * gate and up projections g, u (silu(g) = g * sigmoid(g)).  When g or u is an L
+ * unit, backward uses its reconstruction (App. B.1 Eq. fp8-roundtrip).  Given
+ * the gradient dh, in fp64:
+ *   du = dh * silu(g)
+ *   dg = dh * u * sigmoid(g) * (1 + g * (1 - sigmoid(g)))   (the derivative of silu). */
+void orc_swiglu_bwd(const double *g, const double *u, const double *dh, int64_t n, double *dg,
+                    double *du) {
+  for (int64_t i = 0; i < n; ++i) {
+    const double sg = 1.0 / (1.0 + exp(-g[i]));
+    du[i] = dh[i] * g[i] * sg;
+    dg[i] = dh[i] * u[i] * sg * (1.0 + g[i] * (1.0 - sg));
+  }
+}

@@ -125,6 +125,11 @@ void orc_risk_score(int n_units, const int32_t *unit_class, int n_classes, const
 double orc_update_sparsity(const double *coeff, const uint8_t *flags, const float *adv,
                            const uint8_t *mask, int R, int T, double top_frac, int64_t *counts);
 
+/* ---- backward of the gated MLP activation h = silu(g) * u (fp64):
+ *      du = dh silu(g), dg = dh u silu'(g) */
+void orc_swiglu_bwd(const double *g, const double *u, const double *dh, int64_t n, double *dg,
+                    double *du);
+
 #ifdef __cplusplus
 }
 #endif
