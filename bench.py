@@ -19,8 +19,9 @@ algorithmic bytes (the first figure of the metric); the wgrad TFLOP/s and the
 coefficient tokens/s ride along, each with its own roofline.  For context the
 line also times hilore_allocate (the H/L/R dynamic programme that follows the
 exposure step) on a 196-unit plan, and, under "next", the calls that follow
-the five rows (the LoRA adapter gradient on the MLP unit, the calibration
-scalars, the update-sparsity diagnostics), all outside the step.
+the five rows (the LoRA adapter gradient and the gated-MLP activation backward
+on the MLP unit, the calibration scalars, the update-sparsity diagnostics), all
+outside the step.
 """
 from __future__ import annotations
 
@@ -83,7 +84,8 @@ def measured_traffic():
     common = ["device_common.hpp", "hilore_internal.hpp"]
     files = {"compress": ["codec.hip"], "decompress": ["codec.hip"], "dequant_wgrad": ["wgrad.hip"],
              "grpo_coeffs": ["grpo.hip"], "exposure_risk": ["risk.hip"],
-             "dequant_lora_grad": ["lora.hip"], "grad_rel_err": ["calib.hip"]}
+             "dequant_lora_grad": ["lora.hip"], "grad_rel_err": ["calib.hip"],
+             "dequant_swiglu_bwd": ["swiglu.hip"]}
     out = {}
     for k, ent in table.get("kernels", {}).items():
         h = hashlib.sha256()
@@ -476,6 +478,7 @@ def next_rows_bench(hl, wl, sets, w, code, block, rows, R, iters=20):
       calibrate        hilore_calibrate over 8 calibration microbatches x 196 units
       risk_score       hilore_risk_score for 196 units
       update_sparsity  hilore_update_sparsity on the 16384 coefficient slots
+      swiglu_bwd       hilore_dequant_swiglu_bwd with the MLP unit's codes as the gate
     Each timed with HIP events on the stream it runs on, averaged over `iters`
     calls that rotate over the buffer sets."""
     import numpy as np
@@ -557,6 +560,25 @@ def next_rows_bench(hl, wl, sets, w, code, block, rows, R, iters=20):
 
     ms = timed(sparsity)
     out["update_sparsity_us"] = round(ms * 1e3, 2)
+    # gated-MLP activation backward with the gate in L: the MLP unit's codes as g, its
+    # bf16 activation as u, a bf16 dh of the same shape
+    dh2 = wl.normal_bf16_device(K, M, 600, 0.01)
+    dg = torch.empty((K, M), dtype=torch.bfloat16, device="cuda")
+    du = torch.empty_like(dg)
+
+    def swiglu(i):
+        st = sets[i % len(sets)]
+        x, codes, scales, _, _, _ = st["keep"][1]
+        hl.hilore_dequant_swiglu_bwd(hl.unit_desc(codes=codes, scales=scales, rows=K, cols=M),
+                                     hl.unit_desc(x=x), code, block, dh2, dg, du)
+
+    ms = timed(swiglu)
+    sb = K * M * (1 + 2 + 2 + 4) + K * M * 4 // block
+    out["swiglu_bwd"] = roof("dequant_swiglu_bwd", sb, ms,
+                             f"{sb} B per call: gate codes + scales, up and dh bf16, dgate and dup "
+                             f"bf16, {K}x{M}")
+    out["swiglu_bwd"]["traffic"] = traffic.get("dequant_swiglu_bwd")
+    del dh2, dg, du
     return out
 
 

@@ -12,6 +12,7 @@
  *   in backward     reconstruct L units                     -> hilore_decompress
  *                   and consume them in the weight gradient -> hilore_dequant_wgrad
  *                   or in the LoRA adapter gradient          -> hilore_dequant_lora_grad
+ *                   or in the gated-MLP activation backward  -> hilore_dequant_swiglu_bwd
  * Calibration (App. B.1), before training and between refreshes:
  *   single-unit gradient error y                             -> hilore_grad_rel_err
  *   susceptibility kappa_c and mean reconstruction error     -> hilore_calibrate
@@ -283,6 +284,27 @@ hilore_status hilore_allocate(int n_units, const uint8_t *q, const uint8_t *veri
                               double delta_b, int n_b, int n_d, uint8_t *action, double *totals,
                               int64_t *jk, void *workspace, size_t workspace_bytes,
                               void *stream);
+
+/*
+ * Backward of the gated MLP activation h = silu(g) * u (the MLP of the
+ * evaluated Qwen/Llama models, whose gate and up activations are complete MLP
+ * tensors eligible for L, App. B.1), with an L operand decoded in registers
+ * (App. B.1 Eq. fp8-roundtrip; never written to memory):
+ *   du = dh * silu(g),   dg = dh * u * sigmoid(g) * (1 + g * (1 - sigmoid(g)))
+ *   gate, up   host descriptors of g and u, [rows, cols] each: an L operand gives
+ *              codes (+ scales; not with the cast code) and is decoded to exactly
+ *              the bf16 value hilore_decompress writes; otherwise x is read as bf16
+ *              (row stride ld).  Either or both may be L (then with the same code
+ *              and block); rows and cols must agree.
+ *   dh         bf16 [rows, cols] dense; dgate, dup bf16 [rows, cols] dense outputs
+ * fp32 arithmetic (sigmoid from the hardware exp2 and reciprocal), each output
+ * rounded once to bf16.  Limits: cols % 8 == 0, and cols % block == 0 with an L
+ * operand.  Errors: null pointers, mismatched shapes -> INVALID_ARG; bad
+ * code/block as for hilore_compress; other shapes -> UNSUPPORTED.
+ */
+hilore_status hilore_dequant_swiglu_bwd(const hilore_unit_desc *gate, const hilore_unit_desc *up,
+                                       int code, int block, const uint16_t *dh, uint16_t *dgate,
+                                       uint16_t *dup, void *stream);
 
 /*
  * Relative gradient error of one single-unit L intervention, the calibration

@@ -464,4 +464,47 @@ hilore_status hilore_dequant_lora_grad(const void *x_codes, const float *x_scale
   return hip_status(hilore::launch_lora(a, code, block, r, static_cast<hipStream_t>(stream)));
 }
 
+hilore_status hilore_dequant_swiglu_bwd(const hilore_unit_desc *gate, const hilore_unit_desc *up,
+                                       int code, int block, const uint16_t *dh, uint16_t *dgate,
+                                       uint16_t *dup, void *stream) {
+  if (!gate || !up) return HILORE_ERR_INVALID_ARG;
+  const int64_t rows = gate->rows, cols = gate->cols;
+  if (rows < 0 || cols < 0 || up->rows != rows || up->cols != cols) return HILORE_ERR_INVALID_ARG;
+  const bool gl = gate->codes != nullptr, ul = up->codes != nullptr;
+  if (gl || ul) {
+    const hilore_status cb = check_code_block(code, block);
+    if (cb != HILORE_OK) return cb;
+  }
+  if (cols % 8 != 0 || (block > 0 && (gl || ul) && cols % block != 0)) return HILORE_ERR_UNSUPPORTED;
+  if (rows == 0 || cols == 0) return HILORE_OK;
+  const bool cast = code == HILORE_CODE_FP8_E4M3FN_CAST;
+  const hilore_unit_desc *ops[] = {gate, up};
+  for (const hilore_unit_desc *o : ops) {
+    if (o->codes) {
+      if (!cast && !o->scales) return HILORE_ERR_INVALID_ARG;
+      if (!aligned16(o->codes) || (!cast && !aligned16(o->scales))) return HILORE_ERR_ALIGNMENT;
+    } else {
+      if (!o->x || o->ld < cols) return HILORE_ERR_INVALID_ARG;
+      if (o->ld % 8 != 0 || !aligned16(o->x)) return HILORE_ERR_ALIGNMENT;
+    }
+  }
+  if (!dh || !dgate || !dup) return HILORE_ERR_INVALID_ARG;
+  if (!aligned16(dh) || !aligned16(dgate) || !aligned16(dup)) return HILORE_ERR_ALIGNMENT;
+  hilore::SwigluArgs a{};
+  a.g_x = gl ? nullptr : gate->x;
+  a.u_x = ul ? nullptr : up->x;
+  a.g_codes = static_cast<const uint8_t *>(gate->codes);
+  a.u_codes = static_cast<const uint8_t *>(up->codes);
+  a.g_scales = gl && !cast ? gate->scales : nullptr;
+  a.u_scales = ul && !cast ? up->scales : nullptr;
+  a.g_ld = gate->ld;
+  a.u_ld = up->ld;
+  a.dh = dh;
+  a.dg = dgate;
+  a.du = dup;
+  a.rows = rows;
+  a.cols = cols;
+  return hip_status(hilore::launch_swiglu_bwd(a, code, block, static_cast<hipStream_t>(stream)));
+}
+
 }  // extern "C"

@@ -179,4 +179,16 @@ struct LoraArgs {
 };
 hipError_t launch_lora(const LoraArgs &a, int code, int block, int r, hipStream_t s);
 
+// Backward of the gated MLP activation with an L operand decoded in registers.
+struct SwigluArgs {
+  const uint16_t *g_x, *u_x;       // bf16 operands (row stride g_ld / u_ld), or NULL
+  const uint8_t *g_codes, *u_codes;  // L operands: codes [rows, cols] dense, or NULL
+  const float *g_scales, *u_scales;
+  int64_t g_ld, u_ld;
+  const uint16_t *dh;              // bf16 [rows, cols] dense
+  uint16_t *dg, *du;               // bf16 [rows, cols] dense
+  int64_t rows, cols;
+};
+hipError_t launch_swiglu_bwd(const SwigluArgs &a, int code, int block, hipStream_t s);
+
 }  // namespace hilore

@@ -80,6 +80,7 @@ def load() -> ctypes.CDLL:
         "hilore_lora_grad_workspace_bytes": (ctypes.c_size_t, [i64, i64, i32]),
         "hilore_dequant_lora_grad": (i32, [P, P, i32, i32, P, P, i64, i64, i32, f32, i32, P,
                                            ctypes.c_size_t, P]),
+        "hilore_dequant_swiglu_bwd": (i32, [P, P, i32, i32, P, P, P, P]),
         "hilore_grad_rel_err_workspace_bytes": (ctypes.c_size_t, [i64]),
         "hilore_grad_rel_err": (i32, [P, P, i64, f64, P, P, ctypes.c_size_t, P]),
         "hilore_calibrate": (i32, [i32, i32, i32, P, P, P, P, P, P, P]),
@@ -206,6 +207,16 @@ def hilore_dequant_lora_grad(x_codes, x_scales, code, block: int, dh, da, K: int
                                            _p(dh), _p(da), int(K), int(M), int(r), float(scale),
                                            1 if accumulate else 0, _p(workspace), ws_bytes,
                                            _stream(stream)))
+
+
+def hilore_dequant_swiglu_bwd(gate: hilore_unit_desc, up: hilore_unit_desc, code, block: int, dh,
+                              dgate, dup, stream=None):
+    """dgate, dup (bf16 device tensors) from the gradient dh of h = silu(g) * u; each
+    of gate / up is a unit descriptor: codes (+ scales) for an L operand, x for bf16."""
+    _check("hilore_dequant_swiglu_bwd",
+           load().hilore_dequant_swiglu_bwd(ctypes.byref(gate), ctypes.byref(up), _code(code),
+                                            int(block), _p(dh), _p(dgate), _p(dup),
+                                            _stream(stream)))
 
 
 ACT_R, ACT_H, ACT_L = 0, 1, 2

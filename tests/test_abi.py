@@ -295,3 +295,37 @@ def test_lora_grad_validation(lib):
     for name in ("codes", "scales", "dh", "da", "ws"):
         assert call(**{name: FAKE + 8}) == E.HILORE_ERR_ALIGNMENT, name
     assert call(M=0, da=None) == E.HILORE_OK  # nothing to do
+
+
+def test_swiglu_bwd_validation(lib):
+    E = hilore
+
+    def desc(**kw):
+        d = dict(x=FAKE, codes=None, scales=None, xhat=None, row_ss_x=None, row_ss_err=None,
+                 rows=64, cols=256, ld=256)
+        d.update(kw)
+        return hilore.hilore_unit_desc(d["x"], d["codes"], d["scales"], d["xhat"], d["row_ss_x"],
+                                       d["row_ss_err"], d["rows"], d["cols"], d["ld"])
+
+    def call(g=None, u=None, code=1, block=128, dh=FAKE, dg=FAKE, du=FAKE):
+        g = g if g is not None else desc(x=None, codes=FAKE, scales=FAKE)
+        u = u if u is not None else desc()
+        return lib.hilore_dequant_swiglu_bwd(ctypes.byref(g), ctypes.byref(u), code, block, dh,
+                                             dg, du, None)
+    assert lib.hilore_dequant_swiglu_bwd(None, ctypes.byref(desc()), 1, 128, FAKE, FAKE, FAKE,
+                                         None) == E.HILORE_ERR_INVALID_ARG
+    assert call(u=desc(rows=63)) == E.HILORE_ERR_INVALID_ARG
+    assert call(u=desc(cols=248, ld=256), g=desc(x=None, codes=FAKE, scales=FAKE, cols=248)) == \
+        E.HILORE_ERR_UNSUPPORTED  # cols not a block multiple
+    assert call(g=desc(cols=252, ld=256), u=desc(cols=252, ld=256)) == E.HILORE_ERR_UNSUPPORTED
+    assert call(code=9) == E.HILORE_ERR_INVALID_ARG
+    assert call(block=48) == E.HILORE_ERR_UNSUPPORTED
+    assert call(g=desc(x=None, codes=FAKE, scales=None)) == E.HILORE_ERR_INVALID_ARG
+    assert call(u=desc(x=None)) == E.HILORE_ERR_INVALID_ARG
+    assert call(u=desc(ld=200)) == E.HILORE_ERR_INVALID_ARG
+    assert call(u=desc(ld=260)) == E.HILORE_ERR_ALIGNMENT
+    assert call(u=desc(x=FAKE + 4)) == E.HILORE_ERR_ALIGNMENT
+    assert call(g=desc(x=None, codes=FAKE + 8, scales=FAKE)) == E.HILORE_ERR_ALIGNMENT
+    assert call(dh=None) == E.HILORE_ERR_INVALID_ARG
+    assert call(du=FAKE + 2) == E.HILORE_ERR_ALIGNMENT
+    assert call(g=desc(x=None, codes=FAKE, scales=FAKE, rows=0), u=desc(rows=0)) == E.HILORE_OK
