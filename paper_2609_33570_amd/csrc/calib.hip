@@ -39,10 +39,16 @@ __device__ __forceinline__ double block_sum(double v, double *red) {
 
 // ---------------------------------------------------------------- y ------
 constexpr int kRelThreads = 256;
+constexpr int kRelGroups = 4;  // 16-byte groups per thread and operand in a chunk
+constexpr int64_t kRelChunk = (int64_t)kRelThreads * kRelGroups;  // groups per chunk
+constexpr int kRelFinalThreads = 1024;
 
-// Partial sums of (a - b)^2 and b^2 over a grid-strided range of 16-byte
-// groups; the last n % 4 elements go to workgroup 0.  Each thread keeps four
-// loads in flight per operand.
+// Partial sums of (a - b)^2 and b^2 over chunks of kRelChunk 16-byte groups
+// (16 KiB of each operand): workgroup w takes chunks w, w + grid, ..., which
+// at sizes up to kRelMaxPartials chunks is a single chunk, so the grid is one
+// pass of short-lived workgroups over both arrays.  The last n % 4 elements go
+// to workgroup 0.  A thread issues all 2 * kRelGroups loads of a chunk before
+// using them; inside a chunk thread t takes groups t, t + 256, ...
 __global__ __launch_bounds__(kRelThreads) void rel_err_partial_kernel(const float *a,
                                                                       const float *b, int64_t n,
                                                                       double *part) {
@@ -50,35 +56,27 @@ __global__ __launch_bounds__(kRelThreads) void rel_err_partial_kernel(const floa
   const int64_t n4 = n / 4;
   const float4 *a4 = reinterpret_cast<const float4 *>(a);
   const float4 *b4 = reinterpret_cast<const float4 *>(b);
-  const int64_t stride = (int64_t)gridDim.x * kRelThreads;
   double num = 0.0, den = 0.0;
   auto acc = [&](float x, float y) {
     const double d = (double)x - (double)y;
     num = fma(d, d, num);
     den = fma((double)y, (double)y, den);
   };
-  int64_t i = (int64_t)blockIdx.x * kRelThreads + threadIdx.x;
-  for (; i + 3 * stride < n4; i += 4 * stride) {
-    float4 x[4], y[4];
+  for (int64_t c0 = (int64_t)blockIdx.x * kRelChunk; c0 < n4; c0 += (int64_t)gridDim.x * kRelChunk) {
+    float4 x[kRelGroups], y[kRelGroups];
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
-      x[k] = a4[i + k * stride];
-      y[k] = b4[i + k * stride];
+    for (int k = 0; k < kRelGroups; ++k) {
+      const int64_t i = c0 + k * kRelThreads + threadIdx.x;
+      x[k] = i < n4 ? a4[i] : float4{0.f, 0.f, 0.f, 0.f};
+      y[k] = i < n4 ? b4[i] : float4{0.f, 0.f, 0.f, 0.f};
     }
 #pragma unroll
-    for (int k = 0; k < 4; ++k) {
+    for (int k = 0; k < kRelGroups; ++k) {
       acc(x[k].x, y[k].x);
       acc(x[k].y, y[k].y);
       acc(x[k].z, y[k].z);
       acc(x[k].w, y[k].w);
     }
-  }
-  for (; i < n4; i += stride) {
-    const float4 x = a4[i], y = b4[i];
-    acc(x.x, y.x);
-    acc(x.y, y.y);
-    acc(x.z, y.z);
-    acc(x.w, y.w);
   }
   if (blockIdx.x == 0 && threadIdx.x < n - 4 * n4) acc(a[4 * n4 + threadIdx.x], b[4 * n4 + threadIdx.x]);
   num = block_sum<kRelThreads>(num, red);
@@ -89,16 +87,18 @@ __global__ __launch_bounds__(kRelThreads) void rel_err_partial_kernel(const floa
   }
 }
 
-__global__ __launch_bounds__(kRelThreads) void rel_err_final_kernel(const double *part, int n_part,
-                                                                    double eps_num, float *y) {
-  __shared__ double red[kRelThreads];
+// Thread t adds partials t, t + 1024, ... in order, then a fixed tree.
+__global__ __launch_bounds__(kRelFinalThreads) void rel_err_final_kernel(const double *part,
+                                                                         int n_part, double eps_num,
+                                                                         float *y) {
+  __shared__ double red[kRelFinalThreads];
   double num = 0.0, den = 0.0;
-  for (int i = threadIdx.x; i < n_part; i += kRelThreads) {
+  for (int i = threadIdx.x; i < n_part; i += kRelFinalThreads) {
     num += part[2 * i];
     den += part[2 * i + 1];
   }
-  num = block_sum<kRelThreads>(num, red);
-  den = block_sum<kRelThreads>(den, red);
+  num = block_sum<kRelFinalThreads>(num, red);
+  den = block_sum<kRelFinalThreads>(den, red);
   if (threadIdx.x == 0) y[0] = (float)sqrt(num / (den > eps_num ? den : eps_num));
 }
 
@@ -153,96 +153,193 @@ __global__ __launch_bounds__(kCalThreads) void risk_score_kernel(int n_units,
 // ----------------------------------------------------------- sparsity ------
 constexpr int kSpThreads = 1024;
 constexpr int kSpWaves = kSpThreads / kWave;
+constexpr int kSpBatch = 8;         // slots a thread loads before using them
+constexpr int kSpCache = 32768;     // magnitudes kept in LDS when R*T fits (128 KiB)
+constexpr int64_t kSpChunk = (int64_t)kSpThreads * kSpBatch;
 
-// |omega| of slot (r, t) as its fp32 bit pattern (padding reads 0):
-// non-negative fp32 patterns order like their values.
+// |omega| of slot i as its fp32 bit pattern (padding reads 0): non-negative
+// fp32 patterns order like their values.
 __device__ __forceinline__ uint32_t mag_bits(const SparsityArgs &a, int64_t i) {
   const bool valid = a.mask ? a.mask[i] != 0 : true;
   return valid ? (__float_as_uint(a.coeff[i]) & 0x7FFFFFFFu) : 0u;
 }
 
-// One workgroup.  Pass 1 counts the zero-gradient causes and sums |omega|;
-// four histogram passes over the digits 30..23, 22..15, 14..7 and 6..0 of the
-// magnitude bits find the k-th largest magnitude m_k exactly (radix select);
-// a last pass sums the magnitudes above m_k.  The top-k sum is that sum plus
-// (k - #{above}) copies of m_k, whichever of the tied slots a sort would pick.
-// Waves walk response rows, lanes the token slots of a row.
+// hist[bin] += 1 for every active lane, one LDS add per distinct bin of the
+// wave: the exponent digit of |omega| takes only a few values, and plain
+// atomics from 64 lanes to one address serialise.
+__device__ __forceinline__ void hist_add_wave(uint32_t *hist, uint32_t bin, bool active) {
+  uint64_t todo = __ballot(active);
+  while (todo) {
+    const int leader = __ffsll((unsigned long long)todo) - 1;  // wave-uniform
+    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)bin, leader);
+    const uint64_t same = __ballot(active && bin == b);
+    if ((int)(threadIdx.x % kWave) == leader) atomicAdd(&hist[b], (uint32_t)__popcll(same));
+    todo &= ~same;
+  }
+}
+
+// Radix-select step: with hist over the 256 values of the current digit among
+// the slots matching the prefix found so far, pick the bin holding the
+// krem-th largest of them.  S(b) = #{slots in bins >= b}; the chosen bin is the
+// largest b with S(b) >= krem (bin 0 if none).  256 threads scan suffix sums,
+// the one thread whose bin satisfies the condition publishes the result.
+__device__ __forceinline__ void select_bin(const uint32_t *hist, uint32_t *wtot, int shift,
+                                           uint32_t prefix, long long krem, uint32_t *s_prefix,
+                                           long long *s_krem) {
+  const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
+  uint32_t own = 0, v = 0;
+  if (tid < 256) {
+    own = hist[tid];
+    v = own;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {  // suffix scan inside the wave
+      const uint32_t o = __shfl_down(v, off);
+      if (lane + off < kWave) v += o;
+    }
+    if (lane == 0) wtot[w] = v;
+  }
+  __syncthreads();
+  if (tid < 256) {
+    long long s = v;  // S(tid)
+    for (int w2 = w + 1; w2 < 256 / kWave; ++w2) s += wtot[w2];
+    const long long above = s - own;  // S(tid + 1)
+    if (above < krem && (s >= krem || tid == 0)) {
+      *s_prefix = prefix | ((uint32_t)tid << shift);
+      *s_krem = krem - above;
+    }
+  }
+  __syncthreads();
+}
+
+// Sum over the workgroup in a fixed order: an xor butterfly inside each wave,
+// then wave 0 adds the kSpWaves wave totals in index order; every thread gets
+// the total.  `red` holds kSpWaves doubles.
+__device__ __forceinline__ double sp_block_sum(double v, double *red) {
+  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) v += __shfl_xor(v, off);
+  if (lane == 0) red[w] = v;
+  __syncthreads();
+  double t = 0.0;
+#pragma unroll
+  for (int i = 0; i < kSpWaves; ++i) t += red[i];
+  __syncthreads();
+  return t;
+}
+
+// One workgroup.  The first pass over the slots counts the zero-gradient
+// causes, sums |omega| in fp64, builds the histogram of the exponent digit
+// (bits 30..23 of the magnitude) and, when R*T fits, keeps the magnitudes in
+// LDS.  Three more histogram passes over bits 22..15, 14..7 and 6..0 find the
+// k-th largest magnitude m_k exactly (radix select), a last pass sums the
+// magnitudes above m_k.  The top-k sum is that sum plus (k - #{above}) copies of
+// m_k, whichever of the tied slots a sort would pick.  Slots are walked in
+// chunks of kSpChunk, thread t taking slots t, t + 1024, ... of a chunk.
 __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs a) {
-  __shared__ double red[kSpThreads];
+  __shared__ uint32_t cache[kSpCache];
+  __shared__ double red[kSpWaves];
   __shared__ uint32_t hist[256];
+  __shared__ uint32_t wtot[256 / kWave];
   __shared__ unsigned long long cnt[3];
   __shared__ uint32_t s_prefix;
   __shared__ long long s_krem;
-  const int tid = threadIdx.x, wave = tid / kWave, lane = tid % kWave;
+  const int tid = threadIdx.x, lane = tid % kWave;
+  const int64_t n = (int64_t)a.R * a.T;
+  const bool cached = n <= kSpCache;
   if (tid < 3) cnt[tid] = 0;
+  if (tid < 256) hist[tid] = 0;
   __syncthreads();
-  unsigned long long c_pad = 0, c_zero = 0, c_clip = 0;
+
+  unsigned long long c_pad = 0, c_zero = 0, c_clip = 0;  // wave totals (uniform)
   double total = 0.0;
-  for (int r = wave; r < a.R; r += kSpWaves) {
-    const bool zero_adv = a.adv[r] == 0.0f;
-    for (int t = lane; t < a.T; t += kWave) {
-      const int64_t i = (int64_t)r * a.T + t;
-      const bool valid = a.mask ? a.mask[i] != 0 : true;
-      if (!valid) ++c_pad;
-      else if (zero_adv) ++c_zero;
-      else if (a.flags[i] & 2) ++c_clip;
-      total += (double)__uint_as_float(mag_bits(a, i));
+  for (int64_t c0 = 0; c0 < n; c0 += kSpChunk) {
+    uint32_t m[kSpBatch];
+    bool pad[kSpBatch], zero[kSpBatch], clip[kSpBatch];
+#pragma unroll
+    for (int j = 0; j < kSpBatch; ++j) {
+      const int64_t i = c0 + (int64_t)j * kSpThreads + tid;
+      const bool in = i < n;
+      const bool valid = in && (a.mask ? a.mask[i] != 0 : true);
+      const bool zero_adv = in && a.adv[(uint32_t)i / (uint32_t)a.T] == 0.0f;
+      const bool clipped = in && (a.flags[i] & 2) != 0;
+      m[j] = in ? mag_bits(a, i) : 0u;
+      pad[j] = in && !valid;
+      zero[j] = valid && zero_adv;
+      clip[j] = valid && !zero_adv && clipped;
+    }
+#pragma unroll
+    for (int j = 0; j < kSpBatch; ++j) {
+      const int64_t i = c0 + (int64_t)j * kSpThreads + tid;
+      c_pad += __popcll(__ballot(pad[j]));
+      c_zero += __popcll(__ballot(zero[j]));
+      c_clip += __popcll(__ballot(clip[j]));
+      total += (double)__uint_as_float(m[j]);
+      hist_add_wave(hist, m[j] >> 23, i < n);
+      if (cached && i < n) cache[i] = m[j];
     }
   }
-  atomicAdd(&cnt[0], c_pad);
-  atomicAdd(&cnt[1], c_zero);
-  atomicAdd(&cnt[2], c_clip);
-  total = block_sum<kSpThreads>(total, red);
+  if (lane == 0) {
+    atomicAdd(&cnt[0], c_pad);
+    atomicAdd(&cnt[1], c_zero);
+    atomicAdd(&cnt[2], c_clip);
+  }
+  total = sp_block_sum(total, red);  // its barriers complete hist and cnt
   if (tid < 3) a.counts[tid] = (int64_t)cnt[tid];
   if (!(total > 0.0)) {
     if (tid == 0) a.share[0] = 0.0;
     return;
   }
 
-  constexpr int kShift[4] = {23, 15, 7, 0};
-  constexpr uint32_t kDigit[4] = {0xFFu, 0xFFu, 0xFFu, 0x7Fu};
-  uint32_t prefix = 0, known = 0;  // bits of m_k found so far, and their mask
-  long long krem = a.k;            // rank of m_k among the slots matching `prefix`
+  uint32_t prefix = 0;       // bits of m_k found so far
+  long long krem = a.k;      // rank of m_k among the slots matching `prefix`
+  select_bin(hist, wtot, 23, prefix, krem, &s_prefix, &s_krem);
+  prefix = s_prefix;
+  krem = s_krem;
+  constexpr int kShift[3] = {15, 7, 0};
+  constexpr uint32_t kDigit[3] = {0xFFu, 0xFFu, 0x7Fu};
+  // mask of the bits fixed in `prefix` (bit 31 is 0 in every magnitude)
+  uint32_t known = 0x80000000u | (0xFFu << 23);
 #pragma unroll
-  for (int d = 0; d < 4; ++d) {
+  for (int d = 0; d < 3; ++d) {
     if (tid < 256) hist[tid] = 0;
     __syncthreads();
-    for (int r = wave; r < a.R; r += kSpWaves)
-      for (int t = lane; t < a.T; t += kWave) {
-        const uint32_t m = mag_bits(a, (int64_t)r * a.T + t);
-        if ((m & known) == prefix) atomicAdd(&hist[(m >> kShift[d]) & kDigit[d]], 1u);
+    for (int64_t c0 = 0; c0 < n; c0 += kSpChunk) {
+      uint32_t m[kSpBatch];
+#pragma unroll
+      for (int j = 0; j < kSpBatch; ++j) {
+        const int64_t i = c0 + (int64_t)j * kSpThreads + tid;
+        m[j] = i >= n ? 0xFFFFFFFFu : cached ? cache[i] : mag_bits(a, i);
       }
-    __syncthreads();
-    if (tid == 0) {
-      long long above = 0;
-      int bin = (int)kDigit[d];
-      for (; bin > 0; --bin) {
-        if (above + (long long)hist[bin] >= krem) break;
-        above += hist[bin];
-      }
-      s_prefix = prefix | ((uint32_t)bin << kShift[d]);
-      s_krem = krem - above;
+#pragma unroll
+      for (int j = 0; j < kSpBatch; ++j)  // the all-ones filler never matches: bit 31
+        if ((m[j] & known) == prefix) atomicAdd(&hist[(m[j] >> kShift[d]) & kDigit[d]], 1u);
     }
     __syncthreads();
+    select_bin(hist, wtot, kShift[d], prefix, krem, &s_prefix, &s_krem);
     prefix = s_prefix;
     krem = s_krem;
     known |= kDigit[d] << kShift[d];
   }
   double top = 0.0;
-  for (int r = wave; r < a.R; r += kSpWaves)
-    for (int t = lane; t < a.T; t += kWave) {
-      const uint32_t m = mag_bits(a, (int64_t)r * a.T + t);
-      if (m > prefix) top += (double)__uint_as_float(m);
+  for (int64_t c0 = 0; c0 < n; c0 += kSpChunk) {
+#pragma unroll
+    for (int j = 0; j < kSpBatch; ++j) {
+      const int64_t i = c0 + (int64_t)j * kSpThreads + tid;
+      if (i < n) {
+        const uint32_t m = cached ? cache[i] : mag_bits(a, i);
+        if (m > prefix) top += (double)__uint_as_float(m);
+      }
     }
-  top = block_sum<kSpThreads>(top, red);
+  }
+  top = sp_block_sum(top, red);
   if (tid == 0) a.share[0] = (top + (double)krem * (double)__uint_as_float(prefix)) / total;
 }
 
 }  // namespace
 
 int rel_err_partials(int64_t n) {
-  const int64_t groups = (n / 4 + kRelThreads * 16 - 1) / (kRelThreads * 16);
-  return (int)(groups < 1 ? 1 : (groups > kRelMaxPartials ? kRelMaxPartials : groups));
+  const int64_t chunks = (n / 4 + kRelChunk - 1) / kRelChunk;
+  return (int)(chunks < 1 ? 1 : (chunks > kRelMaxPartials ? kRelMaxPartials : chunks));
 }
 
 hipError_t launch_grad_rel_err(const float *g_l, const float *g_ex, int64_t n, double eps_num,
@@ -250,8 +347,8 @@ hipError_t launch_grad_rel_err(const float *g_l, const float *g_ex, int64_t n, d
   const int np = rel_err_partials(n);
   hipLaunchKernelGGL(rel_err_partial_kernel, dim3(np), dim3(kRelThreads), 0, s, g_l, g_ex, n,
                      part);
-  hipLaunchKernelGGL(rel_err_final_kernel, dim3(1), dim3(kRelThreads), 0, s, part, np, eps_num,
-                     y);
+  hipLaunchKernelGGL(rel_err_final_kernel, dim3(1), dim3(kRelFinalThreads), 0, s, part, np,
+                     eps_num, y);
   return hipGetLastError();
 }
 

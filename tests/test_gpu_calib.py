@@ -68,6 +68,24 @@ def test_grad_rel_err_dw_sized(hl, orc):
     assert abs(float(host(y)[0]) - want) <= 1e-5 * want
 
 
+def test_grad_rel_err_beyond_one_pass(hl, orc):
+    """More 16 KiB chunks than partial slots (4 * 16384 * 1024 floats plus a
+    ragged chunk and a 3-element tail): workgroups then take a second chunk."""
+    n = 4 * 16384 * 1024 + 4096 + 3
+    g = torch.Generator(device="cuda")
+    g.manual_seed(wl.BASE_SEED + 52)
+    ex = torch.randn(n, generator=g, device="cuda")
+    lo = ex + torch.randn(n, generator=g, device="cuda") * 1e-2
+    ws = torch.empty(hl.hilore_grad_rel_err_workspace_bytes(n) // 8, dtype=torch.float64,
+                     device="cuda")
+    assert ws.numel() == 2 * 16384
+    y = filled(1, torch.float32, float("nan"))
+    hl.hilore_grad_rel_err(lo, ex, y, ws)
+    torch.cuda.synchronize()
+    got, want = float(host(y)[0]), orc.grad_rel_err(host(lo), host(ex))
+    assert abs(got - want) <= 1e-5 * want, (got, want)
+
+
 def calib_case(nb, nu, nc, seed):
     rng = wl.rng(seed, 1)
     e = rng.uniform(0.1, 2.0, (nb, nu)).astype(np.float32)
