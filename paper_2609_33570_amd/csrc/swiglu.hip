@@ -11,9 +11,12 @@
 //
 // Elementwise and bound by HBM: per element 2 B of dh, 1 + 4/BLOCK B per L
 // operand or 2 B per bf16 operand, 4 B of outputs.  A thread takes 8
-// consecutive columns of one row (16-byte loads and stores, 8-byte code loads);
-// a workgroup of 256 threads covers 2048 columns of a row, the grid's second
-// dimension walks the rows.
+// consecutive columns of one row (16-byte loads and stores, 8-byte code loads),
+// all touched once, so loads and stores are non-temporal.  A workgroup is one
+// wave covering 512 columns of a row (4.5 KiB at 9 B per element) and the grid
+// is one pass of such short-lived workgroups, columns fastest, rows on the
+// grid's second dimension: on 16384 x 18944 this ran ~17% faster than
+// 256-thread workgroups over 2048 columns.
 #include "device_common.hpp"
 #include "hilore_internal.hpp"
 
@@ -23,45 +26,60 @@
 namespace hilore {
 namespace {
 
-constexpr int kThreads = 256;
+constexpr int kThreads = 64;
 constexpr int kColsPerThread = 8;
 constexpr int kRowGrid = 65535;
 
-// 8 values of one operand at (row, col .. col+7) as fp32.
+// The raw bits of 8 values of one operand at (row, col .. col+7): a bf16
+// operand's 16 bytes, or an L operand's 8 code bytes and its block scale.
+struct Raw {
+  u32x4 w;
+  u32x2 c;
+  float s;
+};
+
 template <int CODE, int BLOCK, bool L>
 __device__ __forceinline__ void load_operand(const uint16_t *x, const uint8_t *codes,
                                              const float *scales, int64_t ld, int64_t cols,
-                                             int64_t row, int64_t col, float v[8]) {
+                                             int64_t row, int64_t col, Raw &r) {
   if constexpr (!L) {
-    const u32x4 w = *reinterpret_cast<const u32x4 *>(x + row * ld + col);
-    v[0] = bf16_lo(w.x); v[1] = bf16_hi(w.x);
-    v[2] = bf16_lo(w.y); v[3] = bf16_hi(w.y);
-    v[4] = bf16_lo(w.z); v[5] = bf16_hi(w.z);
-    v[6] = bf16_lo(w.w); v[7] = bf16_hi(w.w);
+    r.w = __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(x + row * ld + col));
   } else {
-    const u32x2 c = *reinterpret_cast<const u32x2 *>(codes + row * cols + col);
+    r.c = __builtin_nontemporal_load(reinterpret_cast<const u32x2 *>(codes + row * cols + col));
+    if constexpr (CODE != kCodeCast) r.s = scales[row * (cols / BLOCK) + col / BLOCK];
+  }
+}
+
+// The 8 values as fp32: an L operand decoded exactly as decompress does it.
+template <int CODE, bool L>
+__device__ __forceinline__ void decode_operand(const Raw &r, float v[8]) {
+  if constexpr (!L) {
+    v[0] = bf16_lo(r.w.x); v[1] = bf16_hi(r.w.x);
+    v[2] = bf16_lo(r.w.y); v[3] = bf16_hi(r.w.y);
+    v[4] = bf16_lo(r.w.z); v[5] = bf16_hi(r.w.z);
+    v[6] = bf16_lo(r.w.w); v[7] = bf16_hi(r.w.w);
+  } else {
     float q[8];
     if constexpr (CODE == kCodeInt8) {
 #pragma unroll
       for (int i = 0; i < 4; ++i) {
-        q[i] = (float)(int)__builtin_amdgcn_sbfe(c.x, 8 * i, 8);
-        q[4 + i] = (float)(int)__builtin_amdgcn_sbfe(c.y, 8 * i, 8);
+        q[i] = (float)(int)__builtin_amdgcn_sbfe(r.c.x, 8 * i, 8);
+        q[4 + i] = (float)(int)__builtin_amdgcn_sbfe(r.c.y, 8 * i, 8);
       }
     } else {
       f32x2 d;
-      d = __builtin_amdgcn_cvt_pk_f32_fp8((int)c.x, false); q[0] = d.x; q[1] = d.y;
-      d = __builtin_amdgcn_cvt_pk_f32_fp8((int)c.x, true);  q[2] = d.x; q[3] = d.y;
-      d = __builtin_amdgcn_cvt_pk_f32_fp8((int)c.y, false); q[4] = d.x; q[5] = d.y;
-      d = __builtin_amdgcn_cvt_pk_f32_fp8((int)c.y, true);  q[6] = d.x; q[7] = d.y;
+      d = __builtin_amdgcn_cvt_pk_f32_fp8((int)r.c.x, false); q[0] = d.x; q[1] = d.y;
+      d = __builtin_amdgcn_cvt_pk_f32_fp8((int)r.c.x, true);  q[2] = d.x; q[3] = d.y;
+      d = __builtin_amdgcn_cvt_pk_f32_fp8((int)r.c.y, false); q[4] = d.x; q[5] = d.y;
+      d = __builtin_amdgcn_cvt_pk_f32_fp8((int)r.c.y, true);  q[6] = d.x; q[7] = d.y;
     }
     if constexpr (CODE == kCodeCast) {  // exact bf16 values (NaN codes stay NaN)
 #pragma unroll
       for (int i = 0; i < 8; ++i) v[i] = q[i];
     } else {
-      const float s = scales[row * (cols / BLOCK) + col / BLOCK];
 #pragma unroll
       for (int i = 0; i < 8; i += 2) {
-        const uint32_t h = pack_bf16(q[i] * s, q[i + 1] * s);  // xhat, as decompress rounds it
+        const uint32_t h = pack_bf16(q[i] * r.s, q[i + 1] * r.s);  // xhat, as decompress rounds it
         v[i] = bf16_lo(h);
         v[i + 1] = bf16_hi(h);
       }
@@ -75,10 +93,14 @@ __global__ __launch_bounds__(kThreads) void swiglu_bwd_kernel(const SwigluArgs a
   if (col >= a.cols) return;
   constexpr float kLog2e = 1.44269504088896340736f;
   for (int64_t row = blockIdx.y; row < a.rows; row += gridDim.y) {
+    Raw rg, ru;
+    load_operand<CODE, BLOCK, GL>(a.g_x, a.g_codes, a.g_scales, a.g_ld, a.cols, row, col, rg);
+    load_operand<CODE, BLOCK, UL>(a.u_x, a.u_codes, a.u_scales, a.u_ld, a.cols, row, col, ru);
+    const u32x4 dw =
+        __builtin_nontemporal_load(reinterpret_cast<const u32x4 *>(a.dh + row * a.cols + col));
     float g[8], u[8], d[8];
-    load_operand<CODE, BLOCK, GL>(a.g_x, a.g_codes, a.g_scales, a.g_ld, a.cols, row, col, g);
-    load_operand<CODE, BLOCK, UL>(a.u_x, a.u_codes, a.u_scales, a.u_ld, a.cols, row, col, u);
-    const u32x4 dw = *reinterpret_cast<const u32x4 *>(a.dh + row * a.cols + col);
+    decode_operand<CODE, GL>(rg, g);
+    decode_operand<CODE, UL>(ru, u);
     d[0] = bf16_lo(dw.x); d[1] = bf16_hi(dw.x);
     d[2] = bf16_lo(dw.y); d[3] = bf16_hi(dw.y);
     d[4] = bf16_lo(dw.z); d[5] = bf16_hi(dw.z);
@@ -98,8 +120,8 @@ __global__ __launch_bounds__(kThreads) void swiglu_bwd_kernel(const SwigluArgs a
     pg.z = pack_bf16(og[4], og[5]); pg.w = pack_bf16(og[6], og[7]);
     pu.x = pack_bf16(ou[0], ou[1]); pu.y = pack_bf16(ou[2], ou[3]);
     pu.z = pack_bf16(ou[4], ou[5]); pu.w = pack_bf16(ou[6], ou[7]);
-    *reinterpret_cast<u32x4 *>(a.dg + row * a.cols + col) = pg;
-    *reinterpret_cast<u32x4 *>(a.du + row * a.cols + col) = pu;
+    __builtin_nontemporal_store(pg, reinterpret_cast<u32x4 *>(a.dg + row * a.cols + col));
+    __builtin_nontemporal_store(pu, reinterpret_cast<u32x4 *>(a.du + row * a.cols + col));
   }
 }
 
