@@ -31,6 +31,8 @@ import os
 import sys
 import time
 
+from paper_2609_33570_amd import defaults as D
+
 ROOT = os.path.dirname(os.path.abspath(__file__))
 sys.path.insert(0, ROOT)
 
@@ -178,13 +180,13 @@ def main():
                 ev[i].record()
         mark(0)
         hl.hilore_grpo_coeffs(st["rewards"], st["lp_new"], st["lp_old"], None, None, w.P, w.G,
-                              w.T, 0.2, 1e-6, 0.0, 0.0, st["adv"], st["ratio"], st["flags"],
-                              st["coeff"])
+                              w.T, D.CLIP_EPS, D.ADV_EPS, 0.0, 0.0, st["adv"], st["ratio"],
+                              st["flags"], st["coeff"])
         mark(1)
         hl.hilore_compress(st["uc"], code, block)
         mark(2)
-        hl.hilore_unit_exposure_risk(st["coeff"], None, rows, st["uc"], 1e-8, 1e-8, st["expo"],
-                                     st["risk"], st["rel"])
+        hl.hilore_unit_exposure_risk(st["coeff"], None, rows, st["uc"], D.EPS_ALPHA, D.EPS_REL,
+                                     st["expo"], st["risk"], st["rel"])
         mark(3)
         hl.hilore_decompress(st["ud"], code, block)
         mark(4)
@@ -353,12 +355,12 @@ def codec_workload(args, hl, wl):
             if ev is not None:
                 ev[i].record()
         mark(0)
-        hl.hilore_grpo_coeffs(rewards, lp_new, lp_old, None, mask, w.P, w.G, w.T, 0.2, 1e-6,
-                              0.0, 0.0, adv, ratio, flags, coeff)
+        hl.hilore_grpo_coeffs(rewards, lp_new, lp_old, None, mask, w.P, w.G, w.T, D.CLIP_EPS,
+                              D.ADV_EPS, 0.0, 0.0, adv, ratio, flags, coeff)
         mark(1)
         hl.hilore_compress(uc, code, block)
         mark(2)
-        hl.hilore_unit_exposure_risk(coeff, mask, rows, uc, 1e-8, 1e-8, expo, risk, rel)
+        hl.hilore_unit_exposure_risk(coeff, mask, rows, uc, D.EPS_ALPHA, D.EPS_REL, expo, risk, rel)
         mark(3)
         hl.hilore_decompress(ud, code, block)
         mark(4)
@@ -439,7 +441,7 @@ def alloc_bench(hl, wl, iters=10):
     import torch
 
     inst = wl.alloc_instance(wl.qwen2_7b_unit_mix(), seed=wl.BASE_SEED + 3)
-    n_b = n_d = 1024
+    n_b, n_d = D.N_B, D.N_DELTA
     d = [torch.from_numpy(np.ascontiguousarray(a)).cuda() for a in inst.arrays()]
     action = torch.empty(inst.U, dtype=torch.uint8, device="cuda")
     totals = torch.empty(3, dtype=torch.float64, device="cuda")
@@ -505,7 +507,7 @@ def next_rows_bench(hl, wl, sets, w, code, block, rows, R, iters=20):
     out = {}
     # LoRA adapter gradient on the MLP unit of each set
     u = w.units[1]
-    K, M, r = u.rows, u.cols, 16
+    K, M, r = u.rows, u.cols, D.LORA_RANK
     dhs = [wl.normal_bf16_device(K, r, 500 + i, 0.05) for i in range(len(sets))]
     da = torch.empty((r, M), dtype=torch.float32, device="cuda")
     ws = torch.empty(hl.hilore_lora_grad_workspace_bytes(K, M, r), dtype=torch.uint8,
@@ -515,7 +517,7 @@ def next_rows_bench(hl, wl, sets, w, code, block, rows, R, iters=20):
         st = sets[i % len(sets)]
         _, codes, scales, _, _, _ = st["keep"][1]
         hl.hilore_dequant_lora_grad(codes, scales, code, block, dhs[i % len(sets)], da, K, M, r,
-                                    2.0, False, ws)
+                                    D.LORA_SCALE, False, ws)
 
     ms = timed(lora)
     lb = K * M + K * M * 4 // block + K * r * 2 + r * M * 4
@@ -555,8 +557,8 @@ def next_rows_bench(hl, wl, sets, w, code, block, rows, R, iters=20):
 
     def sparsity(i):
         st = sets[i % len(sets)]
-        hl.hilore_update_sparsity(st["coeff"], st["flags"], st["adv"], None, R, rows // R, 0.1,
-                                  counts, share)
+        hl.hilore_update_sparsity(st["coeff"], st["flags"], st["adv"], None, R, rows // R,
+                                  D.TOP_FRAC, counts, share)
 
     ms = timed(sparsity)
     out["update_sparsity_us"] = round(ms * 1e3, 2)
@@ -651,7 +653,7 @@ def cpu_baseline(args, st, w, block, code):
 
     inst = wl.alloc_instance(wl.qwen2_7b_unit_mix(), seed=wl.BASE_SEED + 3)
     t0 = time.perf_counter()
-    oracle.allocate(*inst.arrays(), inst.m_res, inst.delta_b, n_b=1024, n_d=1024)
+    oracle.allocate(*inst.arrays(), inst.m_res, inst.delta_b, n_b=D.N_B, n_d=D.N_DELTA)
     dt_alloc = time.perf_counter() - t0
     # LoRA adapter gradient (rank 16) on the first 256 columns of the MLP unit
     _, mc, msc, _, _, _ = st["keep"][1]
@@ -659,7 +661,7 @@ def cpu_baseline(args, st, w, block, code):
     lsc = msc[:, :256 // block].cpu().contiguous().numpy()
     dh = wl.normal_bf16_host(lc.shape[0], 16, seed=wl.BASE_SEED + 9, sigma=0.05)
     t0 = time.perf_counter()
-    oracle.lora_down_grad(lc, lsc, code, block, dh, scale=2.0, variant=0)
+    oracle.lora_down_grad(lc, lsc, code, block, dh, scale=D.LORA_SCALE, variant=0)
     dt_lora = time.perf_counter() - t0
     lora_bytes = lc.size + lsc.size * 4 + dh.size * 2 + 16 * 256 * 4
     return {

@@ -6,4 +6,4 @@ draws the seeded synthetic inputs.
 """
 from . import workloads  # noqa: F401
 
-__all__ = ["hilore", "workloads"]
+__all__ = ["defaults", "hilore", "workloads"]

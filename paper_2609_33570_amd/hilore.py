@@ -12,6 +12,8 @@ import ctypes
 import os
 from typing import Optional, Sequence
 
+from . import defaults as _d
+
 _PKG = os.path.dirname(os.path.abspath(__file__))
 LIB_PATH = os.path.join(_PKG, "libhilore.so")
 
@@ -222,7 +224,7 @@ def hilore_dequant_swiglu_bwd(gate: hilore_unit_desc, up: hilore_unit_desc, code
 ACT_R, ACT_H, ACT_L = 0, 1, 2
 
 
-def hilore_allocate_workspace_bytes(n_units: int, n_b: int = 1024, n_d: int = 1024) -> int:
+def hilore_allocate_workspace_bytes(n_units: int, n_b: int = _d.N_B, n_d: int = _d.N_DELTA) -> int:
     return int(load().hilore_allocate_workspace_bytes(int(n_units), int(n_b), int(n_d)))
 
 
@@ -244,7 +246,7 @@ def hilore_grad_rel_err_workspace_bytes(n: int) -> int:
     return int(load().hilore_grad_rel_err_workspace_bytes(int(n)))
 
 
-def hilore_grad_rel_err(g_l, g_ex, y, workspace, eps_num: float = 1e-30, stream=None):
+def hilore_grad_rel_err(g_l, g_ex, y, workspace, eps_num: float = _d.EPS_NUM, stream=None):
     """y (a one-element f32 device tensor or view) = relative gradient error of
     g_l against g_ex (f32 device tensors of equal size)."""
     n = int(g_ex.numel())
