@@ -10,10 +10,12 @@
 //
 // Since the mean of a_t does not depend on t,
 //   exposure = sum_{t in T} |omega_t| (a_t + eps) / (sum_{s in T} a_s / |T| + eps),
-// so all six sums are formed in ONE pass over the rows.  One workgroup per
-// unit reads the row sums written by the encoder plus omega and the mask, each
-// thread accumulating a fixed strided subset of rows, followed by a fixed LDS
-// tree: the result does not depend on anything but the inputs.
+// so all six sums are formed in ONE pass over the rows.  One workgroup of 1024
+// threads per unit reads the row sums written by the encoder plus omega and
+// the mask; thread t takes rows t, t + 1024, ... in that order, issuing the
+// loads of kBatch rows before using any, then a butterfly per wave and the 16
+// wave totals added in wave order: the result does not depend on anything but
+// the inputs.
 #include "device_common.hpp"
 #include "hilore_internal.hpp"
 
@@ -24,49 +26,62 @@
 namespace hilore {
 namespace {
 
-constexpr int kThreads = 512;
+constexpr int kThreads = 1024;
+constexpr int kWaves = kThreads / kWave;
 constexpr int kSums = 6;
+constexpr int kBatch = 8;  // rows a thread loads before using them
 
 __global__ __launch_bounds__(kThreads) void exposure_risk_kernel(const RiskBatch b) {
-  __shared__ float red[kSums][kThreads];
+  __shared__ float red[kSums][kWaves];
   const RiskUnit &u = b.u[blockIdx.x];
-  const int tid = threadIdx.x;
+  const int tid = threadIdx.x, lane = tid % kWave, wave = tid / kWave;
   float s_a = 0.f, s_n = 0.f, s_wa = 0.f, s_r = 0.f, s_x = 0.f, s_e = 0.f;
-  for (int64_t t = tid; t < b.rows; t += kThreads) {
-    const float sx = u.ss_x[t];
-    const float se = u.ss_err[t];
-    s_x += sx;
-    s_e += se;
-    const bool valid = b.mask ? b.mask[t] != 0 : true;
-    if (valid) {
-      const float a = sqrtf(sx * u.inv_cols);
-      const float w = fabsf(b.coeff[t]);
-      s_a += a;
-      s_n += 1.0f;
-      s_wa = fmaf(w, a + b.eps_alpha, s_wa);
-      s_r = fmaf(w, sqrtf(se), s_r);
-    }
-  }
-  red[0][tid] = s_a;
-  red[1][tid] = s_n;
-  red[2][tid] = s_wa;
-  red[3][tid] = s_r;
-  red[4][tid] = s_x;
-  red[5][tid] = s_e;
-  __syncthreads();
-  for (int h = kThreads / 2; h > 0; h >>= 1) {
-    if (tid < h) {
+  for (int64_t t0 = 0; t0 < b.rows; t0 += (int64_t)kThreads * kBatch) {
+    float sx[kBatch], se[kBatch], om[kBatch];
+    bool in[kBatch], valid[kBatch];
 #pragma unroll
-      for (int k = 0; k < kSums; ++k) red[k][tid] += red[k][tid + h];
+    for (int j = 0; j < kBatch; ++j) {
+      const int64_t t = t0 + (int64_t)j * kThreads + tid;
+      in[j] = t < b.rows;
+      sx[j] = in[j] ? u.ss_x[t] : 0.f;
+      se[j] = in[j] ? u.ss_err[t] : 0.f;
+      om[j] = in[j] ? b.coeff[t] : 0.f;
+      valid[j] = in[j] && (b.mask ? b.mask[t] != 0 : true);
     }
-    __syncthreads();
+#pragma unroll
+    for (int j = 0; j < kBatch; ++j) {
+      if (!in[j]) continue;
+      s_x += sx[j];
+      s_e += se[j];
+      if (valid[j]) {
+        const float a = sqrtf(sx[j] * u.inv_cols);
+        const float w = fabsf(om[j]);
+        s_a += a;
+        s_n += 1.0f;
+        s_wa = fmaf(w, a + b.eps_alpha, s_wa);
+        s_r = fmaf(w, sqrtf(se[j]), s_r);
+      }
+    }
   }
+  const float v[kSums] = {wave_sum(s_a), wave_sum(s_n), wave_sum(s_wa),
+                          wave_sum(s_r), wave_sum(s_x), wave_sum(s_e)};
+  if (lane == 0) {
+#pragma unroll
+    for (int k = 0; k < kSums; ++k) red[k][wave] = v[k];
+  }
+  __syncthreads();
   if (tid == 0) {
-    const float n = red[1][0];
-    const float expo = n > 0.f ? red[2][0] / (red[0][0] / n + b.eps_alpha) : 0.f;
+    float t[kSums];
+#pragma unroll
+    for (int k = 0; k < kSums; ++k) {
+      t[k] = red[k][0];
+      for (int i = 1; i < kWaves; ++i) t[k] += red[k][i];
+    }
+    const float n = t[1];
+    const float expo = n > 0.f ? t[2] / (t[0] / n + b.eps_alpha) : 0.f;
     b.exposure[blockIdx.x] = expo;
-    b.risk[blockIdx.x] = red[3][0];
-    b.rel_err[blockIdx.x] = sqrtf(red[5][0]) / (sqrtf(red[4][0]) + b.eps_rel);
+    b.risk[blockIdx.x] = t[3];
+    b.rel_err[blockIdx.x] = sqrtf(t[5]) / (sqrtf(t[4]) + b.eps_rel);
   }
 }
 
