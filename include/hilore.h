@@ -157,7 +157,7 @@ hilore_status hilore_grpo_coeffs(const float *rewards, const float *logp_new,
  * cast back (a NaN code makes its row's ss_err NaN).
  * All units of one call are encoded on `stream`; they may differ in shape.
  * Errors: bad code, or block != 0 with the cast code -> INVALID_ARG; other
- * block sizes, or a unit of more than 2^30 rows -> UNSUPPORTED.
+ * block sizes, or a unit of more than 2^30 rows or 2^30 columns -> UNSUPPORTED.
  */
 hilore_status hilore_compress(const hilore_unit_desc *units, int n_units, int code, int block,
                               void *stream);
@@ -205,7 +205,8 @@ hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask,
  * bf16 x bf16 products, fp32 accumulation (MFMA).  xhat is never written to memory.
  * With HILORE_CODE_FP8_E4M3FN_CAST (block = 0, x_scales unused, may be NULL)
  * xhat = value(code) exactly; a NaN code makes its row of dW NaN.
- * Limits: M % block == 0, M % 8 == 0, N % 8 == 0, K >= 0 (K = 0 writes zeros or leaves dw).
+ * Limits: M % block == 0, M % 8 == 0, N % 8 == 0, M and N below 2^22 (else
+ * UNSUPPORTED), K >= 0 (K = 0 writes zeros or leaves dw).
  */
 hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, int code,
                                    int block, const uint16_t *dy, float *dw, int64_t K,

@@ -42,7 +42,8 @@ enum UnitUse : unsigned {
 hilore_status check_unit(const hilore_unit_desc &u, int block, unsigned use) {
   if (u.rows < 0 || u.cols < 0) return HILORE_ERR_INVALID_ARG;
   if (block > 0 && u.cols % block != 0) return HILORE_ERR_UNSUPPORTED;
-  if (u.rows > hilore::kRowsPerLaunch) return HILORE_ERR_UNSUPPORTED;
+  if (u.rows > hilore::kRowsPerLaunch || u.cols > hilore::kMaxCodecCols)
+    return HILORE_ERR_UNSUPPORTED;
   if (u.rows == 0 || u.cols == 0) return HILORE_OK;
   if ((use & kUseX) != 0) {
     if (!u.x) return HILORE_ERR_INVALID_ARG;

@@ -29,6 +29,9 @@ struct CodecUnit {
 // The units of one launch share the number of waves that sweep a row.
 constexpr int kUnitsPerLaunch = 16;
 constexpr int64_t kRowsPerLaunch = int64_t(1) << 30;  // bound on a launch's grid
+// Row lengths the codec kernels support: byte offsets inside a row (2 bytes per
+// bf16 element) and the row's buffer range are 32-bit.
+constexpr int64_t kMaxCodecCols = int64_t(1) << 30;
 struct CodecBatch {
   CodecUnit u[kUnitsPerLaunch];
   int64_t row_begin[kUnitsPerLaunch + 1];  // prefix sum of rows over u[]

@@ -111,6 +111,10 @@ def test_codec_validation(lib, fn):
     assert getattr(lib, fn)(None, 0, 0, 128, None) == E.HILORE_OK
     # empty units are skipped without a launch
     assert codec(lib, fn, [unit(rows=0, codes=None, x=None, xhat=None)]) == E.HILORE_OK
+    # row lengths beyond 2^30 (32-bit in-row byte offsets) and more than 2^30 rows
+    big = (1 << 30) + 128
+    assert codec(lib, fn, [unit(cols=big, ld=big)]) == E.HILORE_ERR_UNSUPPORTED
+    assert codec(lib, fn, [unit(rows=(1 << 30) + 1)]) == E.HILORE_ERR_UNSUPPORTED
 
 
 def test_compress_specific_validation(lib):
@@ -166,6 +170,8 @@ def test_wgrad_validation(lib):
     assert wgrad(lib, dy=None) == E.HILORE_ERR_INVALID_ARG
     assert wgrad(lib, x_scales=FAKE + 4) == E.HILORE_ERR_ALIGNMENT
     assert wgrad(lib, M=0) == E.HILORE_OK
+    assert wgrad(lib, M=1 << 22) == E.HILORE_ERR_UNSUPPORTED    # M, N below 2^22
+    assert wgrad(lib, N=1 << 22) == E.HILORE_ERR_UNSUPPORTED
     # the literal cast: block 0 only, no M % block rule, scales may be NULL
     assert wgrad(lib, code=2) == E.HILORE_ERR_INVALID_ARG
     assert wgrad(lib, code=2, block=0, N=100) == E.HILORE_ERR_UNSUPPORTED
