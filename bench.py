@@ -87,7 +87,7 @@ def measured_traffic():
     files = {"compress": ["codec.hip"], "decompress": ["codec.hip"], "dequant_wgrad": ["wgrad.hip"],
              "grpo_coeffs": ["grpo.hip"], "exposure_risk": ["risk.hip"],
              "dequant_lora_grad": ["lora.hip"], "grad_rel_err": ["calib.hip"],
-             "dequant_swiglu_bwd": ["swiglu.hip"]}
+             "dequant_swiglu_bwd": ["swiglu.hip"], "allocate_dp": ["alloc.hip"]}
     out = {}
     for k, ent in table.get("kernels", {}).items():
         h = hashlib.sha256()
@@ -464,9 +464,17 @@ def alloc_bench(hl, wl, iters=10):
     ms = e0.elapsed_time(e1) / iters
     a = action.cpu().numpy()
     cells = (n_b + 1) * ((n_b + 1 + 63) // 64 * 64)
+    per_unit = cells * 16 + cells // 4  # read the previous table, write the next, 2-bit records
+    achieved = per_unit * inst.U / (ms * 1e-3) / 1e9
     return {"units": inst.U, "grid": [n_b + 1, n_d + 1], "ms": round(ms, 4),
             "us_per_unit": round(ms * 1e3 / inst.U, 3),
-            "table_bytes_per_unit": cells * 16 + cells // 4,
+            "table_bytes_per_unit": per_unit,
+            "roofline": {"kernel": "allocate_dp", "bound": "hbm", "achieved": round(achieved, 2),
+                         "peak": HBM_PEAK_GBS, "unit": "GB/s",
+                         "frac": round(achieved / HBM_PEAK_GBS, 4),
+                         "traffic": measured_traffic().get("allocate_dp"),
+                         "algorithmic": f"{per_unit} B per unit (one DP launch); achieved over "
+                                        "the whole call, launches and backtrack included"},
             "chosen": {"R": int((a == 0).sum()), "H": int((a == 1).sum()),
                        "L": int((a == 2).sum())}}
 
