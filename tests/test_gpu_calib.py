@@ -187,3 +187,23 @@ def test_sparsity_after_coefficients(hl, orc, name, shape, beta, sigma):
     np.testing.assert_array_equal(host(counts), o_counts)
     got = float(host(share)[0])
     assert abs(got - o_share) <= 1e-5 * o_share, (got, o_share)
+
+
+def test_deterministic(hl, orc):
+    """Fixed-order fp64 sums: repeated calls agree bit for bit (the relative
+    error at two sizes with ragged tails, the sparsity counts and share on the
+    path that does not keep the magnitudes in LDS)."""
+    rng = wl.rng(wl.BASE_SEED + 56, 1)
+    for n in (3_000_001, 65_541):
+        b = rng.standard_normal(n).astype(np.float32)
+        a = (b + 1e-2 * rng.standard_normal(n)).astype(np.float32)
+        assert rel_err_gpu(hl, a, b) == rel_err_gpu(hl, a, b)
+    R, T = 64, 1024  # 65536 slots: past the LDS cache, every pass reads memory
+    coeff = (rng.standard_normal(R * T) * 1e-4).astype(np.float32)
+    flags = rng.integers(0, 4, R * T).astype(np.uint8)
+    adv = rng.standard_normal(R).astype(np.float32)
+    c1, s1 = sparsity_gpu(hl, coeff, flags, adv, None, R, T)
+    c2, s2 = sparsity_gpu(hl, coeff, flags, adv, None, R, T)
+    assert np.array_equal(c1, c2) and s1 == s2
+    _, o_share = orc.update_sparsity(coeff.astype(np.float64), flags, adv, None, R, T, 0.1)
+    assert abs(s1 - o_share) <= 1e-12 * o_share

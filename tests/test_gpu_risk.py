@@ -78,3 +78,15 @@ def test_many_units_and_empty_token_set(hl, orc):
     b.mask[:] = 0
     g = gpu_pipeline(hl, b, xs[:3], 0, 64)
     assert (g[0] == 0).all() and (g[1] == 0).all() and (g[2] > 0).all()
+
+
+def test_deterministic(hl, orc):
+    """Fixed-order sums: the whole chain (coefficients, compress with row sums,
+    exposure and risk) run twice on the same inputs agrees bit for bit."""
+    b = wl.grpo_batch(2, 8, 512, seed=43, pad_frac=0.2, delta_sigma=0.1)
+    rows = b.P * b.G * b.T
+    xs = [wl.activation_host(rows, c, seed=500 + i) for i, c in enumerate([1024, 2048, 3584])]
+    first = gpu_pipeline(hl, b, xs, 1, 128)
+    second = gpu_pipeline(hl, b, xs, 1, 128)
+    for name, a1, a2 in zip(["exposure", "risk", "rel_err"], first, second):
+        assert np.array_equal(a1.view(np.uint32), a2.view(np.uint32)), name
