@@ -105,3 +105,22 @@ def test_mlp_shapes(hl, orc, rows, cols):
     assert np.array_equal(host(codes[sel]), c_h)
     check(orc, orc.dequantize(c_h, s_h, orc.E4M3FN, 128), host(u[sel]), host(dh[sel]),
           host(dg[sel]), host(du[sel]))
+
+
+def test_rows_beyond_one_grid_pass(hl, orc):
+    """65572 rows: the grid's row dimension stops at 65535, so the rows past it
+    are taken by a second trip of the kernel's row loop (int8 1x32 gate in L,
+    544 columns: one full and one partial 512-column chunk)."""
+    rows, cols, block = 65535 + 37, 544, 32
+    g = wl.activation_host(rows, cols, seed=170)
+    u = wl.activation_host(rows, cols, seed=171)
+    dh = wl.normal_bf16_host(rows, cols, seed=172, sigma=0.01)
+    c, s = orc.quantize(g, 0, block)
+    ct, st, ut = dev(c), dev(s), dev(u)  # descriptors hold raw pointers: keep the tensors
+    got_g, got_u = run(hl, hl.unit_desc(codes=ct, scales=st, rows=rows, cols=cols),
+                       hl.unit_desc(x=ut), 0, block, dev(dh), rows, cols)
+    pick = np.array([0, 1, 4097, 65533, 65534, 65535, 65536, 65550, rows - 1])
+    xhat = orc.dequantize(c[pick], s[pick], 0, block)
+    check(orc, xhat, u[pick], dh[pick], got_g[pick], got_u[pick])
+    # no row left unwritten (the outputs start as NaN)
+    assert not np.isnan(f32(got_g)).any() and not np.isnan(f32(got_u)).any()
