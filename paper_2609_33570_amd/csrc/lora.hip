@@ -25,7 +25,9 @@
 // Balance and locality.  The (strip, k-step) units are numbered strip-major and
 // dealt to 256 workgroups in equal contiguous ranges (stream-K), so every CU
 // gets the same work whatever the shape; a range meets at most two strips (the
-// grid has at least as many workgroups as strips).  With at least 32 strips the
+// grid has at least as many workgroups as strips).  Units of fewer than 32
+// strips instead split every strip into equal parts, one per workgroup (see
+// lora_plan).  With at least 32 strips the
 // workgroup index is remapped so that the 32 workgroups on one XCD (dispatch is
 // round-robin over the 8 XCDs) take consecutive ranges, i.e. about 1/8 of the
 // strips: the scale lines of those strips and the dh rows (read by every strip)
@@ -337,6 +339,8 @@ __global__ __launch_bounds__(kThreads, 1) void lora_kernel(const LoraArgs a) {
 // first one meeting strip s is floor(((s KS + 1) n_wg - 1) / U) and the last
 // floor(((s + 1) KS n_wg - 1) / U); only the first can have begun in an
 // earlier strip, and then holds this strip's sums in its second slot.
+constexpr int kReduceBatch = 16;
+
 __global__ __launch_bounds__(256) void lora_reduce_kernel(const LoraArgs a) {
   const int64_t idx = (int64_t)blockIdx.x * 256 + threadIdx.x;
   constexpr int kQuads = kStrip / 4;
@@ -354,14 +358,16 @@ __global__ __launch_bounds__(256) void lora_reduce_kernel(const LoraArgs a) {
     const float *base = a.part + rr * kStrip + c4;
     sum = *reinterpret_cast<const f32x4 *>(
         base + (2 * w0 + (range_begin(a, w0) < first ? 1 : 0)) * (int64_t)kPart);
-    for (int64_t w = w0 + 1; w <= w1; w += 4) {
-      f32x4 x[4];
+    // up to 16 partials per round trip (a narrow unit's strip has 16 parts);
+    // the additions stay in ascending workgroup order
+    for (int64_t w = w0 + 1; w <= w1; w += kReduceBatch) {
+      f32x4 x[kReduceBatch];
 #pragma unroll
-      for (int k = 0; k < 4; ++k)
+      for (int k = 0; k < kReduceBatch; ++k)
         x[k] = w + k <= w1 ? *reinterpret_cast<const f32x4 *>(base + 2 * (w + k) * (int64_t)kPart)
                            : f32x4{0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-      for (int k = 0; k < 4; ++k) sum += x[k];
+      for (int k = 0; k < kReduceBatch; ++k) sum += x[k];
     }
   }
   float *out = a.da + (int64_t)(a.r0 + rr) * a.M + col;  // M % 16 == 0: 4 in range
@@ -401,6 +407,19 @@ LoraPlan lora_plan(int64_t K, int64_t M, int r) {
   p.n_wg = p.U < want ? p.U : want;
   // an XCD's share of the strips is at least 1 KB of every row from 32 strips on
   p.xcd_remap = p.n_wg % 8 == 0 && p.S >= 32 ? 1 : 0;
+  // Narrow units (fewer than 32 strips, e.g. a hidden-width input): every strip
+  // is split into `parts` equal ranges, one per workgroup, so no range crosses a
+  // strip (one partial each) and the waves' k-steps come in whole ring pairs.
+  // The pairs per wave are the fewest that S * parts <= 256 workgroups allow,
+  // and `parts` the smallest count that reaches them.  On 16384 x 3584 (14
+  // strips) this gives 224 workgroups of 32 k-steps.
+  if (p.S < 32 && p.KS >= 2 * kWaves) {
+    const int64_t per = 2 * kWaves;  // k-steps of one ring pair of every wave
+    const int64_t pmax = kLoraWorkgroups / p.S;
+    const int64_t pairs = (p.KS + per * pmax - 1) / (per * pmax);
+    const int64_t parts = (p.KS + per * pairs - 1) / (per * pairs);
+    p.n_wg = p.S * parts;
+  }
   p.workspace_bytes = (size_t)(p.n_wg > 0 ? p.n_wg : 1) * 2 * kPart * sizeof(float);
   p.passes = (r + kRows - 1) / kRows;
   return p;

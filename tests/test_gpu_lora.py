@@ -9,8 +9,8 @@ unit) against the oracle.
     on the unrounded dequantisation (variant 0: <= 2e-2), for every code and
     block size;
   - ragged K, M and even adapter ranks 2..40 (several 16-row passes), accumulation,
-    K = 0, and the Qwen2-7B-width MLP unit (16384 x 18944, fp8 1x128, rank 16)
-    on sampled columns.
+    K = 0, and the Qwen2-7B-width MLP and hidden units (16384 x 18944 and
+    16384 x 3584, fp8 1x128, rank 16) on sampled columns.
 """
 import numpy as np
 import pytest
@@ -114,13 +114,16 @@ def test_deterministic(hl, orc):
     assert_bytes_equal(a, b, "repeat")
 
 
-def test_qwen2_7b_mlp_unit(hl, orc):
-    """The Qwen2-7B-width MLP unit at full size (16384 x 18944, fp8 1x128),
-    rank-16 adapter: the first 2048 columns (8 strips) and 24 columns drawn
-    from the rest, against the oracle on codes the oracle recomputes."""
+@pytest.mark.parametrize("M,unit", [(18944, 1), (3584, 0)], ids=["mlp_18944", "hidden_3584"])
+def test_qwen2_7b_units(hl, orc, M, unit):
+    """The Qwen2-7B-width units at full size (16384 x 18944 MLP: 74 strips, the
+    stream-K plan; 16384 x 3584 hidden: 14 strips, one workgroup per strip
+    part), fp8 1x128, rank-16 adapter: the first 2048 columns (8 strips) and
+    24 columns drawn from the rest, against the oracle on codes the oracle
+    recomputes."""
     w = wl.QWEN2_7B_LAYER
-    K, M, r, block, code = 16384, 18944, 16, 128, hl.HILORE_CODE_FP8_E4M3FN
-    x = wl.activation_device(K, M, w.seed * 10 + 1, outliers=w.outliers)
+    K, r, block, code = 16384, 16, 128, hl.HILORE_CODE_FP8_E4M3FN
+    x = wl.activation_device(K, M, w.seed * 10 + unit, outliers=w.outliers)
     codes = torch.empty((K, M), dtype=torch.uint8, device="cuda")
     scales = torch.empty((K, M // block), dtype=torch.float32, device="cuda")
     hl.hilore_compress([hl.unit_desc(x=x, codes=codes, scales=scales)], code, block)
