@@ -110,10 +110,31 @@ def _check(fn: str, status: int) -> None:
         raise HiloreError(fn, status)
 
 
+def _device(t) -> None:
+    if not t.is_cuda:
+        raise ValueError(f"libhilore takes device tensors, got one on {t.device}")
+
+
 def _p(t) -> Optional[int]:
-    """Data pointer of a tensor (None -> NULL)."""
+    """Data pointer of a dense device tensor (None -> NULL).  A host tensor
+    would hand the kernels a host address and a strided view the wrong
+    elements, so both are refused here."""
     if t is None:
         return None
+    _device(t)
+    if not t.is_contiguous():
+        raise ValueError(f"libhilore takes dense tensors, got strides {tuple(t.stride())}")
+    return t.data_ptr()
+
+
+def _p_rows(t) -> Optional[int]:
+    """Data pointer of a row-strided 2-D device tensor (a unit's bf16 x: rows
+    may be padded, elements within a row are contiguous)."""
+    if t is None:
+        return None
+    _device(t)
+    if t.dim() != 2 or (t.shape[1] > 1 and t.stride(1) != 1):
+        raise ValueError(f"x must be 2-D with contiguous rows, got strides {tuple(t.stride())}")
     return t.data_ptr()
 
 
@@ -145,7 +166,7 @@ def unit_desc(x=None, codes=None, scales=None, xhat=None, row_ss_x=None, row_ss_
             cols = x.shape[1]
     if ld is None:
         ld = x.stride(0) if x is not None else cols
-    return hilore_unit_desc(_p(x), _p(codes), _p(scales), _p(xhat), _p(row_ss_x),
+    return hilore_unit_desc(_p_rows(x), _p(codes), _p(scales), _p(xhat), _p(row_ss_x),
                             _p(row_ss_err), int(rows), int(cols), int(ld))
 
 

@@ -335,3 +335,43 @@ def test_swiglu_bwd_validation(lib):
     assert call(dh=None) == E.HILORE_ERR_INVALID_ARG
     assert call(du=FAKE + 2) == E.HILORE_ERR_ALIGNMENT
     assert call(g=desc(x=None, codes=FAKE, scales=FAKE, rows=0), u=desc(rows=0)) == E.HILORE_OK
+
+
+class _FakeDeviceTensor:
+    """Just enough of a device tensor for the binding's marshalling checks."""
+
+    def __init__(self, shape, strides, contiguous):
+        self.is_cuda, self.shape, self._strides, self._contig = True, shape, strides, contiguous
+        self.device = "cuda:0"
+
+    def is_contiguous(self):
+        return self._contig
+
+    def stride(self, dim=None):
+        return self._strides if dim is None else self._strides[dim]
+
+    def dim(self):
+        return len(self.shape)
+
+    def data_ptr(self):
+        return FAKE
+
+
+def test_binding_refuses_host_and_strided_tensors(lib):
+    """A host tensor would give the kernels a host address, a strided view the
+    wrong elements: the binding refuses both before anything reaches the
+    library."""
+    import torch
+    x = torch.zeros(4, 8, dtype=torch.bfloat16)
+    with pytest.raises(ValueError, match="device"):
+        hilore.unit_desc(x=x)
+    with pytest.raises(ValueError, match="device"):
+        hilore.hilore_grad_rel_err(torch.zeros(4), torch.zeros(4), torch.zeros(1),
+                                   torch.zeros(2, dtype=torch.float64))
+    with pytest.raises(ValueError, match="dense"):
+        hilore._p(_FakeDeviceTensor((4, 8), (1, 4), False))  # a transposed view
+    assert hilore._p(_FakeDeviceTensor((4, 8), (8, 1), True)) == FAKE
+    # a unit's x may have padded rows, not strided columns
+    assert hilore._p_rows(_FakeDeviceTensor((4, 8), (16, 1), False)) == FAKE
+    with pytest.raises(ValueError, match="contiguous rows"):
+        hilore._p_rows(_FakeDeviceTensor((4, 8), (1, 4), False))
