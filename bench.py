@@ -103,7 +103,7 @@ def main():
     if args.gpus != 1:
         print(f"bench.py measures one GPU only; --gpus {args.gpus} is not supported "
               "(the hot path shards without communication except one dW reduce-scatter, "
-              "which this build does not implement)", file=sys.stderr)
+              "which this library does not implement)", file=sys.stderr)
         return 2
 
     import numpy as np

@@ -256,7 +256,7 @@ double orc_grpo_loss(const float *adv, const double *logp_new, const float *logp
 
 /* The paper's low-precision action stores an FP8 E4M3FN copy of a bf16
  * activation and casts it back for backward (App. B.1, Eq. fp8-roundtrip).
- * This build uses the scaled reading of that codec: every run of `block`
+ * The scaled reading of that codec is the one used here: every run of `block`
  * consecutive elements of a row gets one fp32 scale.  Step by step, with
  * Q = 127 (int8) or 448 (E4M3FN):
  *   amax = max |x_j| over the block (exact: bf16 widens to fp32 exactly);
