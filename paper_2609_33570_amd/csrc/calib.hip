@@ -41,7 +41,8 @@ __device__ __forceinline__ double block_sum(double v, double *red) {
 constexpr int kRelThreads = 256;
 constexpr int kRelGroups = 4;  // 16-byte groups per thread and operand in a chunk
 constexpr int64_t kRelChunk = (int64_t)kRelThreads * kRelGroups;  // groups per chunk
-constexpr int kRelFinalThreads = 1024;
+constexpr int kRelFinalThreads = 256;
+constexpr int kRelFinalBatch = 8;  // partial pairs a thread loads before adding them
 
 // Partial sums of (a - b)^2 and b^2 over chunks of kRelChunk 16-byte groups
 // (16 KiB of each operand): workgroup w takes chunks w, w + grid, ..., which
@@ -87,19 +88,45 @@ __global__ __launch_bounds__(kRelThreads) void rel_err_partial_kernel(const floa
   }
 }
 
-// Thread t adds partials t, t + 1024, ... in order, then a fixed tree.
+// Thread t adds partials t, t + 256, ... in order (loads issued kRelFinalBatch
+// at a time), then an xor butterfly per wave and the 4 wave totals in order.
 __global__ __launch_bounds__(kRelFinalThreads) void rel_err_final_kernel(const double *part,
                                                                          int n_part, double eps_num,
                                                                          float *y) {
-  __shared__ double red[kRelFinalThreads];
+  __shared__ double red[2][kRelFinalThreads / kWave];
   double num = 0.0, den = 0.0;
-  for (int i = threadIdx.x; i < n_part; i += kRelFinalThreads) {
-    num += part[2 * i];
-    den += part[2 * i + 1];
+  for (int i0 = 0; i0 < n_part; i0 += kRelFinalThreads * kRelFinalBatch) {
+    double2 v[kRelFinalBatch];
+#pragma unroll
+    for (int k = 0; k < kRelFinalBatch; ++k) {
+      const int i = i0 + k * kRelFinalThreads + (int)threadIdx.x;
+      v[k] = i < n_part ? reinterpret_cast<const double2 *>(part)[i] : double2{0.0, 0.0};
+    }
+#pragma unroll
+    for (int k = 0; k < kRelFinalBatch; ++k) {
+      num += v[k].x;
+      den += v[k].y;
+    }
   }
-  num = block_sum<kRelFinalThreads>(num, red);
-  den = block_sum<kRelFinalThreads>(den, red);
-  if (threadIdx.x == 0) y[0] = (float)sqrt(num / (den > eps_num ? den : eps_num));
+#pragma unroll
+  for (int off = kWave / 2; off > 0; off >>= 1) {
+    num += __shfl_xor(num, off);
+    den += __shfl_xor(den, off);
+  }
+  const int lane = threadIdx.x % kWave, w = threadIdx.x / kWave;
+  if (lane == 0) {
+    red[0][w] = num;
+    red[1][w] = den;
+  }
+  __syncthreads();
+  if (threadIdx.x == 0) {
+    double n = red[0][0], d = red[1][0];
+    for (int k = 1; k < kRelFinalThreads / kWave; ++k) {
+      n += red[0][k];
+      d += red[1][k];
+    }
+    y[0] = (float)sqrt(n / (d > eps_num ? d : eps_num));
+  }
 }
 
 // ------------------------------------------------------------ kappa, ebar --
