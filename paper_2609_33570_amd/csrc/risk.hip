@@ -54,12 +54,14 @@ __global__ __launch_bounds__(kThreads) void exposure_risk_kernel(const RiskBatch
       s_x += sx[j];
       s_e += se[j];
       if (valid[j]) {
-        const float a = sqrtf(sx[j] * u.inv_cols);
+        // per-row square roots by the hardware v_sqrt_f32 (within 1 ulp; the
+        // sums are checked to 1e-5 against fp64, not bit for bit)
+        const float a = __builtin_amdgcn_sqrtf(sx[j] * u.inv_cols);
         const float w = fabsf(om[j]);
         s_a += a;
         s_n += 1.0f;
         s_wa = fmaf(w, a + b.eps_alpha, s_wa);
-        s_r = fmaf(w, sqrtf(se[j]), s_r);
+        s_r = fmaf(w, __builtin_amdgcn_sqrtf(se[j]), s_r);
       }
     }
   }
