@@ -191,32 +191,39 @@ __device__ __forceinline__ uint32_t mag_bits(const SparsityArgs &a, int64_t i) {
   return valid ? (__float_as_uint(a.coeff[i]) & 0x7FFFFFFFu) : 0u;
 }
 
-// hist[bin] += 1 for every active lane, one LDS add per distinct bin of the
-// wave: the exponent digit of |omega| takes only a few values, and plain
-// atomics from 64 lanes to one address serialise.
-__device__ __forceinline__ void hist_add_wave(uint32_t *hist, uint32_t bin, bool active) {
-  uint64_t todo = __ballot(active);
-  while (todo) {
-    const int leader = __ffsll((unsigned long long)todo) - 1;  // wave-uniform
-    const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)bin, leader);
-    const uint64_t same = __ballot(active && bin == b);
-    if ((int)(threadIdx.x % kWave) == leader) atomicAdd(&hist[b], (uint32_t)__popcll(same));
-    todo &= ~same;
-  }
+// Row of flat slot i (< 2^31) of rows of T slots: the fp64 product i * (1/T)
+// is within one of the quotient, and one correction step makes it exact.
+__device__ __forceinline__ uint32_t row_of(uint32_t i, uint32_t T, double inv_t) {
+  uint32_t r = (uint32_t)((double)i * inv_t);
+  if (r * T > i) --r;
+  else if ((r + 1) * T <= i) ++r;
+  return r;
 }
 
-// Radix-select step: with hist over the 256 values of the current digit among
-// the slots matching the prefix found so far, pick the bin holding the
-// krem-th largest of them.  S(b) = #{slots in bins >= b}; the chosen bin is the
+// Sum of the waves' private histograms for bin threadIdx.x (< 256), in wave
+// order, clearing them for the next pass.  Plain LDS atomics into one
+// histogram per wave keep the conflicts inside a wave: the exponent digit of
+// abs(omega) takes only a few values.
+__device__ __forceinline__ uint32_t merge_hist(uint32_t (*whist)[256]) {
+  uint32_t s = 0;
+  for (int w = 0; w < kSpWaves; ++w) {
+    s += whist[w][threadIdx.x];
+    whist[w][threadIdx.x] = 0;
+  }
+  return s;
+}
+
+// Radix-select step: with `own` the count of bin threadIdx.x (< 256) of the
+// current digit among the slots matching the prefix found so far, pick the
+// bin holding the krem-th largest of them.  S(b) = #{slots in bins >= b}; the chosen bin is the
 // largest b with S(b) >= krem (bin 0 if none).  256 threads scan suffix sums,
 // the one thread whose bin satisfies the condition publishes the result.
-__device__ __forceinline__ void select_bin(const uint32_t *hist, uint32_t *wtot, int shift,
+__device__ __forceinline__ void select_bin(uint32_t own, uint32_t *wtot, int shift,
                                            uint32_t prefix, long long krem, uint32_t *s_prefix,
                                            long long *s_krem) {
   const int tid = threadIdx.x, lane = tid % kWave, w = tid / kWave;
-  uint32_t own = 0, v = 0;
+  uint32_t v = 0;
   if (tid < 256) {
-    own = hist[tid];
     v = own;
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) {  // suffix scan inside the wave
@@ -265,7 +272,7 @@ __device__ __forceinline__ double sp_block_sum(double v, double *red) {
 __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs a) {
   __shared__ uint32_t cache[kSpCache];
   __shared__ double red[kSpWaves];
-  __shared__ uint32_t hist[256];
+  __shared__ uint32_t whist[kSpWaves][256];  // one histogram per wave
   __shared__ uint32_t wtot[256 / kWave];
   __shared__ unsigned long long cnt[3];
   __shared__ uint32_t s_prefix;
@@ -273,8 +280,10 @@ __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs
   const int tid = threadIdx.x, lane = tid % kWave;
   const int64_t n = (int64_t)a.R * a.T;
   const bool cached = n <= kSpCache;
+  const int wave = tid / kWave;
+  const double inv_t = a.T > 0 ? 1.0 / (double)a.T : 0.0;
   if (tid < 3) cnt[tid] = 0;
-  if (tid < 256) hist[tid] = 0;
+  for (int e = tid; e < kSpWaves * 256; e += kSpThreads) (&whist[0][0])[e] = 0;
   __syncthreads();
 
   unsigned long long c_pad = 0, c_zero = 0, c_clip = 0;  // wave totals (uniform)
@@ -287,7 +296,7 @@ __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs
       const int64_t i = c0 + (int64_t)j * kSpThreads + tid;
       const bool in = i < n;
       const bool valid = in && (a.mask ? a.mask[i] != 0 : true);
-      const bool zero_adv = in && a.adv[(uint32_t)i / (uint32_t)a.T] == 0.0f;
+      const bool zero_adv = in && a.adv[row_of((uint32_t)i, (uint32_t)a.T, inv_t)] == 0.0f;
       const bool clipped = in && (a.flags[i] & 2) != 0;
       m[j] = in ? mag_bits(a, i) : 0u;
       pad[j] = in && !valid;
@@ -301,8 +310,10 @@ __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs
       c_zero += __popcll(__ballot(zero[j]));
       c_clip += __popcll(__ballot(clip[j]));
       total += (double)__uint_as_float(m[j]);
-      hist_add_wave(hist, m[j] >> 23, i < n);
-      if (cached && i < n) cache[i] = m[j];
+      if (i < n) {
+        atomicAdd(&whist[wave][m[j] >> 23], 1u);
+        if (cached) cache[i] = m[j];
+      }
     }
   }
   if (lane == 0) {
@@ -310,7 +321,7 @@ __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs
     atomicAdd(&cnt[1], c_zero);
     atomicAdd(&cnt[2], c_clip);
   }
-  total = sp_block_sum(total, red);  // its barriers complete hist and cnt
+  total = sp_block_sum(total, red);  // its barriers complete whist and cnt
   if (tid < 3) a.counts[tid] = (int64_t)cnt[tid];
   if (!(total > 0.0)) {
     if (tid == 0) a.share[0] = 0.0;
@@ -319,7 +330,7 @@ __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs
 
   uint32_t prefix = 0;       // bits of m_k found so far
   long long krem = a.k;      // rank of m_k among the slots matching `prefix`
-  select_bin(hist, wtot, 23, prefix, krem, &s_prefix, &s_krem);
+  select_bin(tid < 256 ? merge_hist(whist) : 0u, wtot, 23, prefix, krem, &s_prefix, &s_krem);
   prefix = s_prefix;
   krem = s_krem;
   constexpr int kShift[3] = {15, 7, 0};
@@ -328,8 +339,6 @@ __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs
   uint32_t known = 0x80000000u | (0xFFu << 23);
 #pragma unroll
   for (int d = 0; d < 3; ++d) {
-    if (tid < 256) hist[tid] = 0;
-    __syncthreads();
     for (int64_t c0 = 0; c0 < n; c0 += kSpChunk) {
       uint32_t m[kSpBatch];
 #pragma unroll
@@ -339,10 +348,12 @@ __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs
       }
 #pragma unroll
       for (int j = 0; j < kSpBatch; ++j)  // the all-ones filler never matches: bit 31
-        if ((m[j] & known) == prefix) atomicAdd(&hist[(m[j] >> kShift[d]) & kDigit[d]], 1u);
+        if ((m[j] & known) == prefix)
+          atomicAdd(&whist[wave][(m[j] >> kShift[d]) & kDigit[d]], 1u);
     }
     __syncthreads();
-    select_bin(hist, wtot, kShift[d], prefix, krem, &s_prefix, &s_krem);
+    select_bin(tid < 256 ? merge_hist(whist) : 0u, wtot, kShift[d], prefix, krem, &s_prefix,
+               &s_krem);
     prefix = s_prefix;
     krem = s_krem;
     known |= kDigit[d] << kShift[d];
