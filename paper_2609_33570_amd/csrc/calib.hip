@@ -200,10 +200,26 @@ __device__ __forceinline__ uint32_t row_of(uint32_t i, uint32_t T, double inv_t)
   return r;
 }
 
+// Add into the wave's own histogram: the lanes sharing the first active
+// lane's bin are added with one LDS add, the rest one by one.  For the
+// exponent digit this covers both shapes of abs(omega): from a GRPO batch a
+// few bins hold most lanes (plain atomics would serialise on them), from a
+// spread distribution many bins hold a few lanes each (a loop over distinct
+// bins would be long).
+__device__ __forceinline__ void hist_add_wave(uint32_t *hist, uint32_t bin, bool active) {
+  const int lane = threadIdx.x % kWave;
+  const uint64_t todo = __ballot(active);
+  if (!todo) return;
+  const int leader = __ffsll((unsigned long long)todo) - 1;  // wave-uniform
+  const uint32_t b = (uint32_t)__builtin_amdgcn_readlane((int)bin, leader);
+  const uint64_t same = __ballot(active && bin == b);
+  if (lane == leader) atomicAdd(&hist[b], (uint32_t)__popcll(same));
+  if (((todo & ~same) >> lane) & 1u) atomicAdd(&hist[bin], 1u);
+}
+
 // Sum of the waves' private histograms for bin threadIdx.x (< 256), in wave
-// order, clearing them for the next pass.  Plain LDS atomics into one
-// histogram per wave keep the conflicts inside a wave: the exponent digit of
-// abs(omega) takes only a few values.
+// order, clearing them for the next pass.  One histogram per wave keeps the
+// address conflicts of the LDS atomics inside a wave.
 __device__ __forceinline__ uint32_t merge_hist(uint32_t (*whist)[256]) {
   uint32_t s = 0;
   for (int w = 0; w < kSpWaves; ++w) {
@@ -310,10 +326,8 @@ __global__ __launch_bounds__(kSpThreads) void sparsity_kernel(const SparsityArgs
       c_zero += __popcll(__ballot(zero[j]));
       c_clip += __popcll(__ballot(clip[j]));
       total += (double)__uint_as_float(m[j]);
-      if (i < n) {
-        atomicAdd(&whist[wave][m[j] >> 23], 1u);
-        if (cached) cache[i] = m[j];
-      }
+      hist_add_wave(whist[wave], m[j] >> 23, i < n);
+      if (cached && i < n) cache[i] = m[j];
     }
   }
   if (lane == 0) {
