@@ -104,6 +104,19 @@ def test_accumulate_and_empty(hl, orc):
         gpu_lora(hl, empty_c, empty_s, orc.INT8, 64, empty_h, accumulate=True, da0=da0), da0)
 
 
+def test_narrow_unit_accumulate(hl, orc):
+    """A narrow unit (7 strips, 131 k-steps: each strip split into parts of
+    unequal length, one workgroup each) with two 16-row passes, accumulating."""
+    K, M, r = 4096 + 96, 1792, 18
+    x = wl.activation_host(K, M, seed=125, outliers=("channels", 0.005, 30.0))
+    codes, scales = orc.quantize(x, orc.INT8, 64)
+    dh = wl.normal_bf16_host(K, r, seed=126, sigma=0.05)
+    da0 = wl.rng(127, 1).standard_normal((r, M)).astype(np.float32)
+    got = gpu_lora(hl, codes, scales, orc.INT8, 64, dh, accumulate=True, da0=da0)
+    want = da0 + orc.lora_down_grad(codes, scales, orc.INT8, 64, dh, scale=2.0, variant=1)
+    assert rel_fro(got, want) <= 1e-6
+
+
 def test_deterministic(hl, orc):
     K, M, r = 4096, 2048, 16
     x = wl.activation_host(K, M, seed=130)
