@@ -10,8 +10,11 @@
 //   update sparsity          padding / zero-advantage / clipped slot counts and the
 //                              top-k share of sum |omega| (App. D.3, diagnostic replays)
 //
-// Every floating-point sum is fp64 in a fixed order (per-thread strided
-// partial sums, then a fixed LDS tree), with no floating-point atomics.
+// Every floating-point sum is fp64 in a fixed order (per-thread partial sums
+// over a fixed set of elements, then a fixed LDS tree, or a butterfly per wave
+// followed by the wave totals in wave order), with no floating-point atomics;
+// the histograms of the sparsity diagnostic are integer counts, exact in any
+// order.
 #include "device_common.hpp"
 #include "hilore_internal.hpp"
 
