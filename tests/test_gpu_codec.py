@@ -73,6 +73,16 @@ def test_shapes_and_blocks(hl, orc, code, block):
         check_unit(orc, x, r, code, block, what=f"{s}")
 
 
+@pytest.mark.parametrize("code", [0, 1], ids=["int8", "e4m3fn"])
+def test_very_wide_rows(hl, orc, code):
+    """Rows of 131456 columns: the 16 waves of a row each sweep ~16 steps of 8
+    columns per lane, i.e. several rounds of the unrolled loop, and the row
+    ends in a partial 512-column step."""
+    x = wl.activation_host(6, 131072 + 3 * 128, seed=140, outliers=("channels", 0.005, 30.0))
+    (res,) = gpu_codec(hl, [x], code, 128)
+    check_unit(orc, x, res, code, 128, what="very wide")
+
+
 def test_tiny_workload_int8(hl, orc):
     """1024 x 896 bf16 N(0,1) with 1% of entries x20, int8 1x128."""
     x = wl.activation_host(1024, 896, seed=wl.TINY.seed, outliers=("entries", 0.01, 20.0))
