@@ -13,15 +13,16 @@
 //
 // Mapping.  One launch per unit updates the whole grid, one thread per cell
 // (rows k of risk cost, columns j of memory cost, a row padded to a multiple
-// of 64 cells so that a wave covers 64 consecutive cells of one row).  Each
+// of 64 cells so that a wave covers 64 consecutive cells of one row; each XCD
+// takes one contiguous band of cells).  Each
 // cell reads its own value and the two shifted sources from the previous
 // table (fp64, all in the 256 MB infinity cache for grids up to a few
 // thousand squared) and writes its new value; the chosen action (2 bits) is
 // gathered across the wave with two ballots and stored as two 64-bit masks
 // per 64 cells, so the backtracking record of a 1025 x 1025 grid is 279 KB
-// per unit.  A reduction kernel then finds the best terminal cell, and a
-// single thread backtracks through the records and sums the chosen costs in
-// unit order.
+// per unit.  A reduction kernel then finds the best terminal cell, one wave
+// backtracks through the records (four units per round trip), and one wave
+// sums the chosen costs in unit order.
 //
 // Every value is produced by the same fp64 operations in the same order as
 // a plain sequential implementation (one addition per unit along a path,
@@ -103,7 +104,12 @@ __global__ __launch_bounds__(kDpThreads) void dp_kernel(const double *__restrict
                                                          uint64_t *__restrict__ pred,
                                                          const AllocUnitCost *__restrict__ uc,
                                                          int KB, int KD, int S) {
-  const int64_t cell = (int64_t)blockIdx.x * kDpThreads + threadIdx.x;
+  // Workgroups are dealt round-robin to the 8 XCDs; renumber them so that
+  // each XCD updates one contiguous band of the grid in every launch, and
+  // the previous table's band (and most shifted sources) is still in its L2.
+  const int n = (int)gridDim.x, x = (int)blockIdx.x & 7, q = n >> 3, rem = n & 7;
+  const int bid = x * q + (x < rem ? x : rem) + ((int)blockIdx.x >> 3);
+  const int64_t cell = (int64_t)bid * kDpThreads + threadIdx.x;
   const int k = (int)(cell / S), j = (int)(cell % S);
   if (k >= KD) return;  // whole waves: S and the grid are multiples of 64
   const AllocUnitCost c = *uc;
@@ -178,6 +184,30 @@ __global__ __launch_bounds__(kDpThreads) void terminal_partial_kernel(const doub
   if (threadIdx.x == 0) partial[blockIdx.x] = b;
 }
 
+// Action of unit `unit` recorded at cell (j, k).
+__device__ __forceinline__ int record(const uint64_t *pred, int64_t unit, int64_t k, int64_t j,
+                                      int KD, int64_t chunks) {
+  const int64_t w = (unit * KD + k) * chunks + j / kWave;
+  const int bit = (int)(j % kWave);
+  return (int)((pred[2 * w] >> bit) & 1u) | ((int)((pred[2 * w + 1] >> bit) & 1u) << 1);
+}
+
+__device__ __forceinline__ int lane_int(int v, int lane) {
+  return __builtin_amdgcn_readlane(v, lane);
+}
+
+// Backtracking, one wave.  The record of unit i at the current cell decides
+// where the record of unit i - 1 is read, so a walk of one unit per step is
+// a chain of dependent loads.  Each round trip instead loads the records of
+// units i .. i - 3 at every cell the path can reach from the current one
+// (1 + 3 + 9 + 27 = 40 cells, one lane each; lane 1 + 3 + ... + 3^(d-1) + p
+// holds the record of unit i - d after the actions whose base-3 digits,
+// unit i first, spell p; actions R, H, L are 0, 1, 2) and resolves the four
+// actions from registers.  Lanes 0..3 carry the costs of units i .. i - 3
+// and fetch those of the next four units during the same round trip.
+constexpr int kLookUnits = 4;
+constexpr int kLookLanes = 40;
+
 __global__ __launch_bounds__(kFinalThreads) void terminal_backtrack_kernel(
     const AllocArgs a, const Best *partial, int n_partial, const uint64_t *pred,
     const AllocUnitCost *uc, int S, int KD) {
@@ -185,33 +215,116 @@ __global__ __launch_bounds__(kFinalThreads) void terminal_backtrack_kernel(
   for (int p = threadIdx.x; p < n_partial; p += kFinalThreads)
     if (better(partial[p].v, partial[p].i, b.v, b.i)) b = partial[p];
   b = block_best<kFinalThreads>(b);
-  if (threadIdx.x != 0) return;
+  if (threadIdx.x >= kWave) return;
+  const int lane = (int)threadIdx.x;
   int64_t k = b.i / S, j = b.i % S;
-  a.jk[0] = j;
-  a.jk[1] = k;
-  a.totals[0] = b.v;
+  if (lane == 0) {
+    a.jk[0] = j;
+    a.jk[1] = k;
+    a.totals[0] = b.v;
+  }
   const int64_t chunks = S / kWave;
-  for (int i = a.U - 1; i >= 0; --i) {
-    const int64_t w = ((int64_t)i * KD + k) * chunks + j / kWave;
-    const int bit = (int)(j % kWave);
-    const int act = (int)((pred[2 * w] >> bit) & 1u) | ((int)((pred[2 * w + 1] >> bit) & 1u) << 1);
-    a.action[i] = (uint8_t)act;
-    if (act == kActH) j -= uc[i].b_h;
-    if (act == kActL) {
-      j -= uc[i].b_l;
-      k -= uc[i].r_l;
+  // this lane's depth d and path p
+  const int d = lane == 0 ? 0 : lane < 4 ? 1 : lane < 13 ? 2 : 3;
+  const int p = lane - (d == 0 ? 0 : d == 1 ? 1 : d == 2 ? 4 : 13);
+  auto load_costs = [&](int unit, int &bh, int &bl, int &rl) {
+    bh = bl = rl = 0;
+    if (lane < kLookUnits && unit - lane >= 0) {
+      const AllocUnitCost c = uc[unit - lane];
+      bh = c.b_h;
+      bl = c.b_l;
+      rl = c.r_l;
     }
+  };
+  int bh, bl, rl;
+  load_costs(a.U - 1, bh, bl, rl);
+  for (int i = a.U - 1; i >= 0; i -= kLookUnits) {
+    int nbh, nbl, nrl;
+    load_costs(i - kLookUnits, nbh, nbl, nrl);
+    // the cell of this lane's record: the current cell minus the costs of
+    // the actions its path takes at units i .. i - d + 1
+    int64_t jj = j, kk = k;
+    int rest = p;
+    int pw = d == 3 ? 9 : d == 2 ? 3 : 1;
+#pragma unroll
+    for (int m = 0; m < 3; ++m) {
+      const int ubh = lane_int(bh, m), ubl = lane_int(bl, m), url = lane_int(rl, m);
+      if (m < d) {
+        const int digit = rest / pw;
+        rest -= digit * pw;
+        pw /= 3;
+        if (digit == kActH) jj -= ubh;
+        if (digit == kActL) {
+          jj -= ubl;
+          kk -= url;
+        }
+      }
+    }
+    int act = kActR;
+    if (lane < kLookLanes && i - d >= 0 && jj >= 0 && kk >= 0)
+      act = record(pred, i - d, kk, jj, KD, chunks);
+    const int a0 = lane_int(act, 0);
+    const int a1 = lane_int(act, 1 + a0);
+    const int a2 = lane_int(act, 4 + 3 * a0 + a1);
+    const int a3 = lane_int(act, 13 + 9 * a0 + 3 * a1 + a2);
+    const int mine = lane == 0 ? a0 : lane == 1 ? a1 : lane == 2 ? a2 : a3;
+    if (lane < kLookUnits && i - lane >= 0) a.action[i - lane] = (uint8_t)mine;
+    const int acts[4] = {a0, a1, a2, a3};
+#pragma unroll
+    for (int m = 0; m < kLookUnits; ++m) {
+      const int ubh = lane_int(bh, m), ubl = lane_int(bl, m), url = lane_int(rl, m);
+      if (i - m >= 0) {
+        if (acts[m] == kActH) j -= ubh;
+        if (acts[m] == kActL) {
+          j -= ubl;
+          k -= url;
+        }
+      }
+    }
+    bh = nbh;
+    bl = nbl;
+    rl = nrl;
   }
+}
+
+__device__ __forceinline__ double lane_f64(double v, int lane) {
+  const uint64_t u = __builtin_bit_cast(uint64_t, v);
+  const uint32_t lo = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)u, lane);
+  const uint32_t hi = (uint32_t)__builtin_amdgcn_readlane((int)(uint32_t)(u >> 32), lane);
+  return __builtin_bit_cast(double, ((uint64_t)hi << 32) | lo);
+}
+
+// Memory and risk of the chosen actions, summed in unit order (one wave:
+// the inputs of 64 units are loaded at once, the additions stay sequential).
+__global__ __launch_bounds__(kWave) void totals_kernel(const AllocArgs a) {
+  const int lane = (int)threadIdx.x;
   double mem = 0.0, risk = 0.0;
-  for (int i = 0; i < a.U; ++i) {
-    if (a.action[i] == kActH) mem += a.dm_h[i];
-    if (a.action[i] == kActL) {
-      mem += a.dm_l[i];
-      risk += a.psi[i];
+  for (int base = 0; base < a.U; base += kWave) {
+    const int u = base + lane;
+    int act = kActR;
+    double cm = 0.0, cr = 0.0;
+    if (u < a.U) {
+      act = a.action[u];
+      if (act == kActH) cm = a.dm_h[u];
+      if (act == kActL) {
+        cm = a.dm_l[u];
+        cr = a.psi[u];
+      }
+    }
+    const int n = a.U - base < kWave ? a.U - base : kWave;
+    for (int t = 0; t < n; ++t) {
+      const int at = lane_int(act, t);
+      if (at == kActH) mem += lane_f64(cm, t);
+      if (at == kActL) {
+        mem += lane_f64(cm, t);
+        risk += lane_f64(cr, t);
+      }
     }
   }
-  a.totals[1] = mem;
-  a.totals[2] = risk;
+  if (lane == 0) {
+    a.totals[1] = mem;
+    a.totals[2] = risk;
+  }
 }
 
 }  // namespace
@@ -256,6 +369,7 @@ hipError_t launch_allocate(const AllocArgs &a, int KB, int KD, void *workspace, 
                      f[a.U & 1], l.cells, partial);
   hipLaunchKernelGGL(terminal_backtrack_kernel, dim3(1), dim3(kFinalThreads), 0, s, a, partial,
                      n_partial, pred, uc, l.S, KD);
+  hipLaunchKernelGGL(totals_kernel, dim3(1), dim3(kWave), 0, s, a);
   return hipGetLastError();
 }
 
