@@ -295,31 +295,39 @@ __device__ __forceinline__ double lane_f64(double v, int lane) {
 }
 
 // Memory and risk of the chosen actions, summed in unit order (one wave:
-// the inputs of 64 units are loaded at once, the additions stay sequential).
+// the inputs of 64 units are loaded at once, one chunk ahead, and the
+// additions stay sequential).  A unit whose action adds nothing adds +0.0,
+// which leaves the sums unchanged: they start at +0.0 and every chosen cost
+// is finite and non-negative, so neither sum is ever -0.0.
+struct UnitTotals {
+  double mem, risk;
+};
+
+__device__ __forceinline__ UnitTotals unit_costs(const AllocArgs &a, int u) {
+  UnitTotals c{0.0, 0.0};
+  if (u < a.U) {
+    const int act = a.action[u];
+    if (act == kActH) c.mem = a.dm_h[u];
+    if (act == kActL) {
+      c.mem = a.dm_l[u];
+      c.risk = a.psi[u];
+    }
+  }
+  return c;
+}
+
 __global__ __launch_bounds__(kWave) void totals_kernel(const AllocArgs a) {
   const int lane = (int)threadIdx.x;
   double mem = 0.0, risk = 0.0;
+  UnitTotals c = unit_costs(a, lane);
   for (int base = 0; base < a.U; base += kWave) {
-    const int u = base + lane;
-    int act = kActR;
-    double cm = 0.0, cr = 0.0;
-    if (u < a.U) {
-      act = a.action[u];
-      if (act == kActH) cm = a.dm_h[u];
-      if (act == kActL) {
-        cm = a.dm_l[u];
-        cr = a.psi[u];
-      }
-    }
+    const UnitTotals next = unit_costs(a, base + kWave + lane);
     const int n = a.U - base < kWave ? a.U - base : kWave;
     for (int t = 0; t < n; ++t) {
-      const int at = lane_int(act, t);
-      if (at == kActH) mem += lane_f64(cm, t);
-      if (at == kActL) {
-        mem += lane_f64(cm, t);
-        risk += lane_f64(cr, t);
-      }
+      mem += lane_f64(c.mem, t);
+      risk += lane_f64(c.risk, t);
     }
+    c = next;
   }
   if (lane == 0) {
     a.totals[1] = mem;
