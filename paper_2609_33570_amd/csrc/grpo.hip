@@ -19,6 +19,9 @@
 // has to be counted, every workgroup counts the whole mask itself (bytes
 // summed four at a time with a dot product), which keeps the launch single
 // and needs no scratch memory; the mask is a few tens of KB and stays in L2.
+// Every load a thread makes is issued before the first arithmetic (the mask
+// words for the count in batches of 8 per thread), so the launch waits on
+// memory about once instead of once per phase.
 #include "device_common.hpp"
 #include "hilore_internal.hpp"
 
@@ -33,6 +36,7 @@ constexpr int kThreads = 256;
 constexpr int kSlotsPerThread = 4;
 constexpr int kSlotsPerBlock = kThreads * kSlotsPerThread;
 constexpr int kMaxResp = kSlotsPerBlock + 2;  // responses overlapping one run (T >= 1)
+constexpr int kMaskBatch = 8;  // 16-byte mask words per thread in flight while counting
 
 // Pairwise-tree sum over the first P2 lanes (P2 a power of two <= 64) by an
 // xor butterfly; lanes >= P2 must not be mixed in, so the loop stops at P2/2.
@@ -66,6 +70,49 @@ __global__ __launch_bounds__(kThreads) void grpo_kernel(const GrpoArgs a, int p2
   const int64_t g_lo = j_lo / a.G;
   const int64_t g_hi = j_hi / a.G;
 
+  // ---- loads first ----
+  // Nothing below changes what a thread reads, so its token slots and the
+  // first batch of mask words for the count are requested before any
+  // arithmetic: the whole prologue then waits on memory about once.
+  const int i0 = (int)c0 + tid * kSlotsPerThread;  // P*G*T < 2^31
+  const bool has_slots = !no_tokens && i0 < c1;
+  float sn[4] = {0.f, 0.f, 0.f, 0.f}, so[4] = {0.f, 0.f, 0.f, 0.f}, sref[4] = {0.f, 0.f, 0.f, 0.f};
+  uint32_t mk = 0x01010101u;
+  const bool full = i0 + kSlotsPerThread <= c1;
+  if (has_slots) {
+    if (full) {
+      const float4 n4 = *reinterpret_cast<const float4 *>(a.logp_new + i0);
+      const float4 o4 = *reinterpret_cast<const float4 *>(a.logp_old + i0);
+      sn[0] = n4.x; sn[1] = n4.y; sn[2] = n4.z; sn[3] = n4.w;
+      so[0] = o4.x; so[1] = o4.y; so[2] = o4.z; so[3] = o4.w;
+      if (a.beta != 0.0f) {
+        const float4 r4 = *reinterpret_cast<const float4 *>(a.logp_ref + i0);
+        sref[0] = r4.x; sref[1] = r4.y; sref[2] = r4.z; sref[3] = r4.w;
+      }
+      if (a.mask) mk = *reinterpret_cast<const uint32_t *>(a.mask + i0);
+    } else {
+      mk = 0;
+      for (int k = 0; k < kSlotsPerThread; ++k) {
+        const int i = i0 + k;
+        const bool in = i < c1;
+        sn[k] = in ? a.logp_new[i] : 0.0f;
+        so[k] = in ? a.logp_old[i] : 0.0f;
+        if (a.beta != 0.0f) sref[k] = in ? a.logp_ref[i] : 0.0f;
+        const uint32_t m = in ? (a.mask ? a.mask[i] : 1u) : 0u;
+        mk |= m << (8 * k);
+      }
+    }
+  }
+  const bool count_words = !no_tokens && a.count_mask && a.mask;
+  const int64_t n_words = count_words ? n_slots / 16 : 0;
+  const uint4 *m4 = reinterpret_cast<const uint4 *>(a.mask);
+  uint4 mw[kMaskBatch];
+#pragma unroll
+  for (int u = 0; u < kMaskBatch; ++u) {
+    const int64_t i = (int64_t)u * kThreads + tid;
+    mw[u] = i < n_words ? m4[i] : make_uint4(0u, 0u, 0u, 0u);
+  }
+
   // ---- advantages of the groups this run touches ----
   for (int64_t grp = g_lo + wave; grp <= g_hi; grp += kThreads / kWave) {
     const int64_t j = grp * a.G + lane;
@@ -88,11 +135,18 @@ __global__ __launch_bounds__(kThreads) void grpo_kernel(const GrpoArgs a, int p2
   if (a.count_mask) {
     uint32_t cnt = 0;
     if (a.mask) {
-      const int64_t n_words = n_slots / 16;
-      const uint4 *m4 = reinterpret_cast<const uint4 *>(a.mask);
-      for (int64_t i = tid; i < n_words; i += kThreads) {
-        const uint4 w = m4[i];
-        cnt += nonzero_bytes(w.x) + nonzero_bytes(w.y) + nonzero_bytes(w.z) + nonzero_bytes(w.w);
+      for (int64_t base = 0; base < n_words; base += kMaskBatch * kThreads) {
+        if (base > 0) {  // later batches: all loads of a batch in flight at once
+#pragma unroll
+          for (int u = 0; u < kMaskBatch; ++u) {
+            const int64_t i = base + (int64_t)u * kThreads + tid;
+            mw[u] = i < n_words ? m4[i] : make_uint4(0u, 0u, 0u, 0u);
+          }
+        }
+#pragma unroll
+        for (int u = 0; u < kMaskBatch; ++u)
+          cnt += nonzero_bytes(mw[u].x) + nonzero_bytes(mw[u].y) + nonzero_bytes(mw[u].z) +
+                 nonzero_bytes(mw[u].w);
       }
       for (int64_t i = n_words * 16 + tid; i < n_slots; i += kThreads) cnt += a.mask[i] != 0;
     } else {
@@ -108,33 +162,7 @@ __global__ __launch_bounds__(kThreads) void grpo_kernel(const GrpoArgs a, int p2
   }
 
   // ---- per-token quantities ----
-  const int i0 = (int)c0 + tid * kSlotsPerThread;  // P*G*T < 2^31
-  if (i0 >= c1) return;
-  float sn[4], so[4], sref[4] = {0.f, 0.f, 0.f, 0.f};
-  uint32_t mk = 0x01010101u;
-  const bool full = i0 + kSlotsPerThread <= c1;
-  if (full) {
-    const float4 n4 = *reinterpret_cast<const float4 *>(a.logp_new + i0);
-    const float4 o4 = *reinterpret_cast<const float4 *>(a.logp_old + i0);
-    sn[0] = n4.x; sn[1] = n4.y; sn[2] = n4.z; sn[3] = n4.w;
-    so[0] = o4.x; so[1] = o4.y; so[2] = o4.z; so[3] = o4.w;
-    if (a.beta != 0.0f) {
-      const float4 r4 = *reinterpret_cast<const float4 *>(a.logp_ref + i0);
-      sref[0] = r4.x; sref[1] = r4.y; sref[2] = r4.z; sref[3] = r4.w;
-    }
-    if (a.mask) mk = *reinterpret_cast<const uint32_t *>(a.mask + i0);
-  } else {
-    mk = 0;
-    for (int k = 0; k < kSlotsPerThread; ++k) {
-      const int i = i0 + k;
-      const bool in = i < c1;
-      sn[k] = in ? a.logp_new[i] : 0.0f;
-      so[k] = in ? a.logp_old[i] : 0.0f;
-      if (a.beta != 0.0f) sref[k] = in ? a.logp_ref[i] : 0.0f;
-      const uint32_t m = in ? (a.mask ? a.mask[i] : 1u) : 0u;
-      mk |= m << (8 * k);
-    }
-  }
+  if (!has_slots) return;
 
   float rat[4], om[4];
   uint32_t fl = 0;
