@@ -72,10 +72,12 @@ def test_given_normaliser(hl, orc):
 
 
 @pytest.mark.parametrize("P,G,T", [(3, 5, 7), (1, 1, 9), (2, 64, 33), (7, 3, 1), (5, 8, 0),
-                                   (1, 2, 4099), (129, 8, 1)])
+                                   (1, 2, 4099), (129, 8, 1), (3, 7, 1601), (5, 9, 1499)])
 def test_odd_shapes(hl, orc, P, G, T):
     """Ragged tails, non-power-of-two groups, G = 1 and 64, T = 1 and T = 0
-    (advantages only)."""
+    (advantages only).  3 x 7 x 1601 and 5 x 9 x 1499 slots make the mask
+    count read a partial second (third) batch of 16-byte words and a byte
+    tail."""
     b = wl.grpo_batch(P, G, T, seed=P * 1000 + G * 10 + T, delta_sigma=0.2,
                       pad_frac=0.25 if T > 1 else None)
     if T == 0:
