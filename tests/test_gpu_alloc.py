@@ -109,3 +109,13 @@ def test_workspace_reuse(hl, orc):
     b = wl.alloc_small(13, seed=12, scale=64.0)
     assert_same(gpu_allocate(hl, a, 512, 512, ws), oracle_allocate(orc, a, 512, 512), "first")
     assert_same(gpu_allocate(hl, b, 300, 500, ws), oracle_allocate(orc, b, 300, 500), "second")
+
+
+@pytest.mark.parametrize("integer", [False, True], ids=["real", "integer"])
+def test_many_units(hl, orc, integer):
+    """1001 units on a 64 x 48 grid: 251 backtracking round trips of four units
+    (the last one partial) and 16 chunks of the in-order cost sums (the last
+    one partial)."""
+    inst = wl.alloc_small(1001, seed=4242 + integer, integer=integer, scale=8.0)
+    assert_same(gpu_allocate(hl, inst, 64, 48), oracle_allocate(orc, inst, 64, 48),
+                f"U=1001 integer={integer}")
