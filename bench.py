@@ -160,6 +160,8 @@ def main():
         st["expo"] = torch.empty(len(w.units), dtype=torch.float32, device="cuda")
         st["risk"] = torch.empty_like(st["expo"])
         st["rel"] = torch.empty_like(st["expo"])
+        st["risk_ws"] = torch.empty(hl.hilore_unit_exposure_risk_workspace_bytes(rows, len(w.units)),
+                                    dtype=torch.uint8, device="cuda")
         # wgrad operands: X stored as fp8-e4m3 1x128 (encoded here, outside the timed region)
         xw = wl.activation_device(K, M, ww.seed + 1000 * s)
         wc = torch.empty((K, M), dtype=torch.uint8, device="cuda")
@@ -186,7 +188,7 @@ def main():
         hl.hilore_compress(st["uc"], code, block)
         mark(2)
         hl.hilore_unit_exposure_risk(st["coeff"], None, rows, st["uc"], D.EPS_ALPHA, D.EPS_REL,
-                                     st["expo"], st["risk"], st["rel"])
+                                     st["expo"], st["risk"], st["rel"], workspace=st["risk_ws"])
         mark(3)
         hl.hilore_decompress(st["ud"], code, block)
         mark(4)
@@ -347,6 +349,10 @@ def codec_workload(args, hl, wl):
     expo = torch.empty(n, dtype=torch.float32, device="cuda")
     risk = torch.empty(n, dtype=torch.float32, device="cuda")
     rel = torch.empty(n, dtype=torch.float32, device="cuda")
+    risk_ws = torch.empty(hl.hilore_unit_exposure_risk_workspace_bytes(rows, n), dtype=torch.uint8,
+                          device="cuda")
+    grpo_ws = torch.empty(max(16, hl.hilore_grpo_coeffs_workspace_bytes(w.P, w.G, w.T)),
+                          dtype=torch.uint8, device="cuda")
     torch.cuda.synchronize()
     names = ["grpo_coeffs", "compress", "exposure_risk", "decompress"]
 
@@ -356,11 +362,12 @@ def codec_workload(args, hl, wl):
                 ev[i].record()
         mark(0)
         hl.hilore_grpo_coeffs(rewards, lp_new, lp_old, None, mask, w.P, w.G, w.T, D.CLIP_EPS,
-                              D.ADV_EPS, 0.0, 0.0, adv, ratio, flags, coeff)
+                              D.ADV_EPS, 0.0, 0.0, adv, ratio, flags, coeff, workspace=grpo_ws)
         mark(1)
         hl.hilore_compress(uc, code, block)
         mark(2)
-        hl.hilore_unit_exposure_risk(coeff, mask, rows, uc, D.EPS_ALPHA, D.EPS_REL, expo, risk, rel)
+        hl.hilore_unit_exposure_risk(coeff, mask, rows, uc, D.EPS_ALPHA, D.EPS_REL, expo, risk, rel,
+                                     workspace=risk_ws)
         mark(3)
         hl.hilore_decompress(ud, code, block)
         mark(4)

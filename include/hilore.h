@@ -129,13 +129,22 @@ int hilore_version(void);
  *                               0 where m_t = 0 or N = 0
  * chi_t is decided in log-ratio space: delta = s_t - s_t^old (fp32), chi = delta <= log1p(eps)
  * when A >= 0, else delta >= log1p(-eps), both thresholds rounded to fp32.
+ * workspace: used only to count N (n_norm <= 0 with a mask) over more than 2^16
+ * slots: then device memory of at least hilore_grpo_coeffs_workspace_bytes(P, G, T)
+ * bytes (4 bytes per 2^16 slots, at most 1 KB), 16-byte aligned, contents on entry
+ * irrelevant, and calls sharing it must not overlap; otherwise it may be NULL (the
+ * query returns 0 for at most 2^16 slots).
  * Limits: 1 <= G <= 64, P >= 0, T >= 0, P*G*T < 2^31.
+ * Errors: bad eps or beta, NaN n_norm, null pointers -> INVALID_ARG; G > 64 or too
+ * many slots -> UNSUPPORTED; workspace too small when it is needed -> WORKSPACE.
  */
+size_t hilore_grpo_coeffs_workspace_bytes(int P, int G, int T);
 hilore_status hilore_grpo_coeffs(const float *rewards, const float *logp_new,
                                  const float *logp_old, const float *logp_ref,
                                  const uint8_t *mask, int P, int G, int T, float clip_eps,
                                  float adv_eps, float beta, double n_norm, float *adv,
-                                 float *ratio, uint8_t *flags, float *coeff, void *stream);
+                                 float *ratio, uint8_t *flags, float *coeff, void *workspace,
+                                 size_t workspace_bytes, void *stream);
 
 /*
  * Blockwise absmax encode of the L candidates after forward (App. B.1 Eq.
@@ -184,14 +193,26 @@ hilore_status hilore_decompress(const hilore_unit_desc *units, int n_units, int 
  *   risk[u]     = sum_{t in T} |omega_t| sqrt(ss_err_t)
  *   rel_err[u]  = sqrt(sum_t ss_err_t) / (sqrt(sum_t ss_x_t) + eps_rel)   (all rows)
  * exposure and risk are 0 when T is empty.  Outputs are device f32 [n_units].
+ * The sums are fp32: partial sums over chunks of 2048 rows of each unit go to
+ * `workspace` and are then added in a fixed order (no floating-point atomics,
+ * so repeated calls give identical bits).
+ * workspace: device memory of at least hilore_unit_exposure_risk_workspace_bytes(rows,
+ * n_units) bytes (32 bytes per unit per 2048 rows; 0, and then NULL is allowed, when
+ * rows == 0), 16-byte aligned, contents on entry irrelevant; calls sharing it must
+ * not overlap.
  * The calibrated risk of App. B.1 Eq. app-risk-score is kappa * exposure * mean rel_err
  * and the additive distortion of Eq. app-distortion sums it over L units; both are
  * host-side scalar steps.
+ * Limits: rows < 2^24 (else UNSUPPORTED).  Errors: negative sizes or eps, null
+ * pointers, a unit whose rows differ from `rows` -> INVALID_ARG; workspace too
+ * small -> WORKSPACE.
  */
+size_t hilore_unit_exposure_risk_workspace_bytes(int64_t rows, int n_units);
 hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask, int64_t rows,
                                         const hilore_unit_desc *units, int n_units,
                                         float eps_alpha, float eps_rel, float *exposure,
-                                        float *risk, float *rel_err, void *stream);
+                                        float *risk, float *rel_err, void *workspace,
+                                        size_t workspace_bytes, void *stream);
 
 /*
  * Weight gradient of a linear layer whose saved input is an L unit, with the

@@ -129,6 +129,70 @@ hilore_status run_codec(const hilore_unit_desc *units, int n_units, int code, in
   return flush();
 }
 
+// Workspace of hilore_grpo_coeffs: the pre-pass counts, when n slots need one.
+size_t grpo_workspace_bytes(int64_t n) {
+  return (size_t)hilore::grpo_count_blocks(n) * sizeof(uint32_t);
+}
+
+size_t risk_workspace_bytes(int64_t rows, int n_units) {
+  return (size_t)n_units * (size_t)hilore::risk_chunks(rows) * hilore::kRiskPartFloats *
+         sizeof(float);
+}
+
+// Arguments of hilore_unit_exposure_risk other than the workspace.
+hilore_status check_exposure_risk(const float *coeff, const uint8_t *mask, int64_t rows,
+                                  const hilore_unit_desc *units, int n_units, float eps_alpha,
+                                  float eps_rel, const float *exposure, const float *risk,
+                                  const float *rel_err) {
+  if (rows < 0 || n_units < 0) return HILORE_ERR_INVALID_ARG;
+  if (!(eps_alpha >= 0.0f) || !(eps_rel >= 0.0f)) return HILORE_ERR_INVALID_ARG;
+  if (n_units == 0) return HILORE_OK;
+  if (!units || !exposure || !risk || !rel_err) return HILORE_ERR_INVALID_ARG;
+  if (rows >= hilore::kRiskMaxRows) return HILORE_ERR_UNSUPPORTED;
+  if (rows > 0 && !coeff) return HILORE_ERR_INVALID_ARG;
+  if ((coeff && !aligned16(coeff)) || (mask && !aligned16(mask))) return HILORE_ERR_ALIGNMENT;
+  const void *outs[] = {exposure, risk, rel_err};  // written one float at a time
+  for (const void *p : outs)
+    if ((reinterpret_cast<uintptr_t>(p) & 3u) != 0) return HILORE_ERR_ALIGNMENT;
+  for (int i = 0; i < n_units; ++i) {
+    const hilore_unit_desc &u = units[i];
+    if (u.rows != rows || u.cols <= 0) return HILORE_ERR_INVALID_ARG;
+    if (rows > 0) {
+      const hilore_status st = check_unit(u, 0, kNeedStats);
+      if (st != HILORE_OK) return st;
+    }
+  }
+  return HILORE_OK;
+}
+
+// Partial sums of every (row chunk, unit) into part ([unit][chunk] layout),
+// then one fold launch over all units.
+hilore_status run_exposure_risk(const float *coeff, const uint8_t *mask, int64_t rows,
+                                const hilore_unit_desc *units, int n_units, float eps_alpha,
+                                float eps_rel, float *exposure, float *risk, float *rel_err,
+                                float *part, hipStream_t s) {
+  const int64_t n_chunks = hilore::risk_chunks(rows);
+  for (int first = 0; first < n_units && n_chunks > 0; first += hilore::kRiskUnitsPerLaunch) {
+    hilore::RiskBatch b{};
+    b.coeff = coeff;
+    b.mask = mask;
+    b.rows = rows;
+    b.n_chunks = n_chunks;
+    b.eps_alpha = eps_alpha;
+    b.part = part + (int64_t)first * n_chunks * hilore::kRiskPartFloats;
+    for (int i = first; i < n_units && b.n < hilore::kRiskUnitsPerLaunch; ++i) {
+      b.ss_x[b.n] = units[i].row_ss_x;
+      b.ss_err[b.n] = units[i].row_ss_err;
+      b.inv_cols[b.n] = (float)(1.0 / (double)units[i].cols);
+      ++b.n;
+    }
+    const hilore_status st = hip_status(hilore::launch_risk_partial(b, s));
+    if (st != HILORE_OK) return st;
+  }
+  return hip_status(hilore::launch_risk_fold(part, n_units, n_chunks, eps_alpha, eps_rel,
+                                             exposure, risk, rel_err, s));
+}
+
 }  // namespace
 
 extern "C" {
@@ -147,11 +211,17 @@ const char *hilore_status_string(int status) {
 
 int hilore_version(void) { return 10000; }
 
+size_t hilore_grpo_coeffs_workspace_bytes(int P, int G, int T) {
+  if (P < 0 || G < 1 || T < 0) return 0;
+  return grpo_workspace_bytes((int64_t)P * G * (int64_t)T);
+}
+
 hilore_status hilore_grpo_coeffs(const float *rewards, const float *logp_new,
                                  const float *logp_old, const float *logp_ref,
                                  const uint8_t *mask, int P, int G, int T, float clip_eps,
                                  float adv_eps, float beta, double n_norm, float *adv,
-                                 float *ratio, uint8_t *flags, float *coeff, void *stream) {
+                                 float *ratio, uint8_t *flags, float *coeff, void *workspace,
+                                 size_t workspace_bytes, void *stream) {
   if (P < 0 || T < 0 || G < 1) return HILORE_ERR_INVALID_ARG;
   if (G > 64) return HILORE_ERR_UNSUPPORTED;
   const int64_t R = (int64_t)P * G;
@@ -169,6 +239,13 @@ hilore_status hilore_grpo_coeffs(const float *rewards, const float *logp_new,
     const void *ptrs[] = {logp_new, logp_old, logp_ref, mask, ratio, flags, coeff};
     for (const void *p : ptrs)
       if (p && !aligned16(p)) return HILORE_ERR_ALIGNMENT;
+  }
+  // a pre-pass counts N into the workspace when no N is given for a large masked call
+  const bool pre_count = n > 0 && n_norm <= 0.0 && mask && hilore::grpo_count_blocks(n) > 0;
+  if (pre_count) {
+    if (!workspace) return HILORE_ERR_INVALID_ARG;
+    if (!aligned16(workspace)) return HILORE_ERR_ALIGNMENT;
+    if (workspace_bytes < grpo_workspace_bytes(n)) return HILORE_ERR_WORKSPACE;
   }
   hilore::GrpoArgs a{};
   a.rewards = rewards;
@@ -189,7 +266,8 @@ hilore_status hilore_grpo_coeffs(const float *rewards, const float *logp_new,
   a.beta = beta;
   a.count_mask = n_norm > 0.0 ? 0 : 1;
   a.inv_n = n_norm > 0.0 ? (float)(1.0 / n_norm) : 0.0f;
-  return hip_status(hilore::launch_grpo(a, static_cast<hipStream_t>(stream)));
+  return hip_status(hilore::launch_grpo(a, pre_count ? static_cast<uint32_t *>(workspace) : nullptr,
+                                        static_cast<hipStream_t>(stream)));
 }
 
 hilore_status hilore_compress(const hilore_unit_desc *units, int n_units, int code, int block,
@@ -208,49 +286,26 @@ hilore_status hilore_decompress(const hilore_unit_desc *units, int n_units, int 
                    [&](const CodecBatch &b) { return hilore::launch_decompress(b, code, block, s); });
 }
 
+size_t hilore_unit_exposure_risk_workspace_bytes(int64_t rows, int n_units) {
+  if (rows < 0 || n_units < 0 || rows >= hilore::kRiskMaxRows) return 0;
+  return risk_workspace_bytes(rows, n_units);
+}
+
 hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask, int64_t rows,
                                         const hilore_unit_desc *units, int n_units,
                                         float eps_alpha, float eps_rel, float *exposure,
-                                        float *risk, float *rel_err, void *stream) {
-  if (rows < 0 || n_units < 0) return HILORE_ERR_INVALID_ARG;
-  if (!(eps_alpha >= 0.0f) || !(eps_rel >= 0.0f)) return HILORE_ERR_INVALID_ARG;
-  if (n_units == 0) return HILORE_OK;
-  if (!units || !exposure || !risk || !rel_err) return HILORE_ERR_INVALID_ARG;
-  if (rows >= (int64_t(1) << 24)) return HILORE_ERR_UNSUPPORTED;
-  if (rows > 0 && !coeff) return HILORE_ERR_INVALID_ARG;
-  if ((coeff && !aligned16(coeff)) || (mask && !aligned16(mask))) return HILORE_ERR_ALIGNMENT;
-  const void *outs[] = {exposure, risk, rel_err};  // written one float at a time
-  for (const void *p : outs)
-    if ((reinterpret_cast<uintptr_t>(p) & 3u) != 0) return HILORE_ERR_ALIGNMENT;
-  for (int i = 0; i < n_units; ++i) {
-    const hilore_unit_desc &u = units[i];
-    if (u.rows != rows || u.cols <= 0) return HILORE_ERR_INVALID_ARG;
-    if (rows > 0) {
-      const hilore_status st = check_unit(u, 0, kNeedStats);
-      if (st != HILORE_OK) return st;
-    }
-  }
-  hipStream_t s = static_cast<hipStream_t>(stream);
-  for (int first = 0; first < n_units; first += hilore::kRiskUnitsPerLaunch) {
-    hilore::RiskBatch b{};
-    b.coeff = coeff;
-    b.mask = mask;
-    b.rows = rows;
-    b.eps_alpha = eps_alpha;
-    b.eps_rel = eps_rel;
-    b.exposure = exposure + first;
-    b.risk = risk + first;
-    b.rel_err = rel_err + first;
-    for (int i = first; i < n_units && b.n < hilore::kRiskUnitsPerLaunch; ++i) {
-      b.u[b.n].ss_x = units[i].row_ss_x;
-      b.u[b.n].ss_err = units[i].row_ss_err;
-      b.u[b.n].inv_cols = (float)(1.0 / (double)units[i].cols);
-      ++b.n;
-    }
-    const hilore_status st = hip_status(hilore::launch_exposure_risk(b, s));
-    if (st != HILORE_OK) return st;
-  }
-  return HILORE_OK;
+                                        float *risk, float *rel_err, void *workspace,
+                                        size_t workspace_bytes, void *stream) {
+  const hilore_status st = check_exposure_risk(coeff, mask, rows, units, n_units, eps_alpha,
+                                               eps_rel, exposure, risk, rel_err);
+  if (st != HILORE_OK || n_units == 0) return st;
+  const size_t need = risk_workspace_bytes(rows, n_units);
+  if (need > 0 && !workspace) return HILORE_ERR_INVALID_ARG;
+  if (workspace && !aligned16(workspace)) return HILORE_ERR_ALIGNMENT;
+  if (workspace_bytes < need) return HILORE_ERR_WORKSPACE;
+  return run_exposure_risk(coeff, mask, rows, units, n_units, eps_alpha, eps_rel, exposure, risk,
+                           rel_err, static_cast<float *>(workspace),
+                           static_cast<hipStream_t>(stream));
 }
 
 hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, int code,

@@ -10,17 +10,22 @@
 //             (Eq. update-coefficient with the K3 KL derivative of the proof of
 //             Prop. 1)
 //
-// One launch.  Each workgroup owns a run of 1024 consecutive token slots
+// Each workgroup of grpo_kernel owns a run of 1024 consecutive token slots
 // (4 per thread, 128-bit loads).  It first forms, with wave butterflies, the
 // advantages of every group its slots touch (a group of G <= 64 rewards sits
 // in the lanes of one wave; the group sums are the pairwise tree over the
 // next power of two >= G, which the xor butterfly produces exactly) and keeps
-// them in LDS; then every thread processes its 4 slots elementwise.  When N
-// has to be counted, every workgroup counts the whole mask itself (bytes
-// summed four at a time with a dot product), which keeps the launch single
-// and needs no scratch memory; the mask is a few tens of KB and stays in L2.
+// them in LDS; then every thread processes its 4 slots elementwise.
+// When N has to be counted (no N given, a mask present), calls of at most
+// kGrpoCountInKernelSlots slots let every workgroup count the whole mask
+// itself (bytes summed four at a time with a dot product): one launch, no
+// scratch, and the mask (at most 64 KB) stays in L2.  Larger calls first run
+// count_kernel, whose workgroups each count one contiguous range of the mask
+// into the caller's workspace (one 32-bit count each, at most kGrpoCounts),
+// and every workgroup of grpo_kernel then adds those counts (exact integer
+// sums): the mask is read once more in total instead of once per workgroup.
 // Every load a thread makes is issued before the first arithmetic (the mask
-// words for the count in batches of 8 per thread), so the launch waits on
+// words or counts for N in batches of 8 per thread), so a launch waits on
 // memory about once instead of once per phase.
 #include "device_common.hpp"
 #include "hilore_internal.hpp"
@@ -37,6 +42,7 @@ constexpr int kSlotsPerThread = 4;
 constexpr int kSlotsPerBlock = kThreads * kSlotsPerThread;
 constexpr int kMaxResp = kSlotsPerBlock + 2;  // responses overlapping one run (T >= 1)
 constexpr int kMaskBatch = 8;  // 16-byte mask words per thread in flight while counting
+static_assert(kGrpoCounts <= kThreads, "one pre-pass count per thread");
 
 // Pairwise-tree sum over the first P2 lanes (P2 a power of two <= 64) by an
 // xor butterfly; lanes >= P2 must not be mixed in, so the loop stops at P2/2.
@@ -50,6 +56,38 @@ __device__ __forceinline__ uint32_t nonzero_bytes(uint32_t w) {
   w |= w >> 2;
   w |= w >> 1;
   return __builtin_amdgcn_udot4(w & 0x01010101u, 0x01010101u, 0u, false);
+}
+
+// Count of the nonzero bytes of mask words [w0, w1) plus, in the last
+// workgroup, of the bytes past the last whole word; one 32-bit count per
+// workgroup.
+__global__ __launch_bounds__(kThreads) void count_kernel(const uint8_t *mask, int64_t n_slots,
+                                                         int64_t words_per_wg, uint32_t *counts) {
+  __shared__ uint32_t red[kThreads / kWave];
+  const int tid = threadIdx.x, lane = tid & (kWave - 1), wave = tid / kWave;
+  const int64_t n_words = n_slots / 16;
+  const int64_t w0 = (int64_t)blockIdx.x * words_per_wg;
+  const int64_t w1 = w0 + words_per_wg < n_words ? w0 + words_per_wg : n_words;
+  const uint4 *m4 = reinterpret_cast<const uint4 *>(mask);
+  uint32_t cnt = 0;
+  for (int64_t base = w0; base < w1; base += kMaskBatch * kThreads) {
+    uint4 mw[kMaskBatch];
+#pragma unroll
+    for (int u = 0; u < kMaskBatch; ++u) {
+      const int64_t i = base + (int64_t)u * kThreads + tid;
+      mw[u] = i < w1 ? m4[i] : make_uint4(0u, 0u, 0u, 0u);
+    }
+#pragma unroll
+    for (int u = 0; u < kMaskBatch; ++u)
+      cnt += nonzero_bytes(mw[u].x) + nonzero_bytes(mw[u].y) + nonzero_bytes(mw[u].z) +
+             nonzero_bytes(mw[u].w);
+  }
+  if (blockIdx.x == gridDim.x - 1)
+    for (int64_t i = n_words * 16 + tid; i < n_slots; i += kThreads) cnt += mask[i] != 0;
+  for (int off = 1; off < kWave; off <<= 1) cnt += __shfl_xor(cnt, off, kWave);
+  if (lane == 0) red[wave] = cnt;
+  __syncthreads();
+  if (tid == 0) counts[blockIdx.x] = red[0] + red[1] + red[2] + red[3];
 }
 
 __global__ __launch_bounds__(kThreads) void grpo_kernel(const GrpoArgs a, int p2) {
@@ -103,7 +141,10 @@ __global__ __launch_bounds__(kThreads) void grpo_kernel(const GrpoArgs a, int p2
       }
     }
   }
-  const bool count_words = !no_tokens && a.count_mask && a.mask;
+  // counts of a count_kernel pre-pass (one per thread at most), else the mask itself
+  uint32_t pre = 0;
+  if (!no_tokens && a.count_mask && a.counts && tid < a.n_counts) pre = a.counts[tid];
+  const bool count_words = !no_tokens && a.count_mask && a.mask && !a.counts;
   const int64_t n_words = count_words ? n_slots / 16 : 0;
   const uint4 *m4 = reinterpret_cast<const uint4 *>(a.mask);
   uint4 mw[kMaskBatch];
@@ -134,7 +175,9 @@ __global__ __launch_bounds__(kThreads) void grpo_kernel(const GrpoArgs a, int p2
   float inv_n = a.inv_n;
   if (a.count_mask) {
     uint32_t cnt = 0;
-    if (a.mask) {
+    if (a.counts) {
+      cnt = pre;
+    } else if (a.mask) {
       for (int64_t base = 0; base < n_words; base += kMaskBatch * kThreads) {
         if (base > 0) {  // later batches: all loads of a batch in flight at once
 #pragma unroll
@@ -199,14 +242,36 @@ __global__ __launch_bounds__(kThreads) void grpo_kernel(const GrpoArgs a, int p2
 
 }  // namespace
 
-hipError_t launch_grpo(const GrpoArgs &a, hipStream_t s) {
+int grpo_count_blocks(int64_t slots) {
+  if (slots <= kGrpoCountInKernelSlots) return 0;
+  const int64_t n = (slots + kGrpoSlotsPerCount - 1) / kGrpoSlotsPerCount;
+  return (int)(n < kGrpoCounts ? n : kGrpoCounts);
+}
+
+hipError_t launch_grpo(const GrpoArgs &a, uint32_t *counts, hipStream_t s) {
   const int64_t R = (int64_t)a.P * a.G;
   const int64_t slots = a.T == 0 ? R : R * a.T;
   if (slots == 0) return hipSuccess;
   int p2 = 1;
   while (p2 < a.G) p2 <<= 1;
+  GrpoArgs b = a;
+  b.counts = nullptr;
+  b.n_counts = 0;
+  if (a.T > 0 && a.count_mask && a.mask && counts) {
+    const int nb = grpo_count_blocks(slots);
+    if (nb > 0) {  // counted by a pre-pass into the workspace
+      const int64_t n_words = slots / 16;
+      const int64_t per = (n_words + nb - 1) / nb;
+      hipLaunchKernelGGL(count_kernel, dim3((unsigned)nb), dim3(kThreads), 0, s, a.mask, slots,
+                         per, counts);
+      const hipError_t e = hipGetLastError();
+      if (e != hipSuccess) return e;
+      b.counts = counts;
+      b.n_counts = nb;
+    }
+  }
   const int64_t grid = (slots + kSlotsPerBlock - 1) / kSlotsPerBlock;
-  hipLaunchKernelGGL(grpo_kernel, dim3((unsigned)grid), dim3(kThreads), 0, s, a, p2);
+  hipLaunchKernelGGL(grpo_kernel, dim3((unsigned)grid), dim3(kThreads), 0, s, b, p2);
   return hipGetLastError();
 }
 

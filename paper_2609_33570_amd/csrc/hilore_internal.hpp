@@ -57,25 +57,31 @@ inline int codec_wpr_log2(int64_t cols, int lane_steps) {
 hipError_t launch_compress(const CodecBatch &b, int code, int block, hipStream_t s);
 hipError_t launch_decompress(const CodecBatch &b, int code, int block, hipStream_t s);
 
-struct RiskUnit {
-  const float *ss_x;
-  const float *ss_err;
-  float inv_cols;  // 1 / d_u
-};
-constexpr int kRiskUnitsPerLaunch = 32;
+// Exposure / risk: workgroup (chunk, unit) sums kRiskChunkRows rows of one
+// unit into six fp32 partials of kRiskPartFloats floats (padded for 16-byte
+// stores), laid out [unit][chunk]; a second launch folds them per unit.
+constexpr int kRiskRowsPerThread = 8;
+constexpr int64_t kRiskChunkRows = 256 * kRiskRowsPerThread;
+constexpr int kRiskPartFloats = 8;
+constexpr int64_t kRiskMaxRows = int64_t(1) << 24;  // keeps the valid-row count exact in fp32
+constexpr int kRiskUnitsPerLaunch = 96;  // units per partial launch (by value in the arguments)
 struct RiskBatch {
-  RiskUnit u[kRiskUnitsPerLaunch];
-  float *exposure;  // already offset to the first unit of this launch
-  float *risk;
-  float *rel_err;
+  const float *ss_x[kRiskUnitsPerLaunch];
+  const float *ss_err[kRiskUnitsPerLaunch];
+  float inv_cols[kRiskUnitsPerLaunch];  // 1 / d_u
+  float *part;                          // partials of this launch's first unit
   const float *coeff;
   const uint8_t *mask;
   int64_t rows;
+  int64_t n_chunks;
   float eps_alpha;
-  float eps_rel;
   int n;
 };
-hipError_t launch_exposure_risk(const RiskBatch &b, hipStream_t s);
+int64_t risk_chunks(int64_t rows);
+hipError_t launch_risk_partial(const RiskBatch &b, hipStream_t s);
+hipError_t launch_risk_fold(const float *part, int n_units, int64_t n_chunks, float eps_alpha,
+                            float eps_rel, float *exposure, float *risk, float *rel_err,
+                            hipStream_t s);
 
 struct GrpoArgs {
   const float *rewards, *logp_new, *logp_old, *logp_ref;
@@ -87,8 +93,18 @@ struct GrpoArgs {
   float adv_eps, beta;
   float inv_n;        // 1/N when N is given
   int count_mask;     // N = number of valid slots in this call
+  const uint32_t *counts;  // set by launch_grpo: pre-pass counts of the mask, or NULL
+  int n_counts;
 };
-hipError_t launch_grpo(const GrpoArgs &a, hipStream_t s);
+// Counting N: up to kGrpoCountInKernelSlots slots every workgroup counts the
+// mask itself; beyond, a pre-pass of grpo_count_blocks(slots) workgroups (one
+// per kGrpoSlotsPerCount slots, at most kGrpoCounts) writes one uint32 count
+// each into the caller's workspace.
+constexpr int64_t kGrpoCountInKernelSlots = int64_t(1) << 16;
+constexpr int64_t kGrpoSlotsPerCount = int64_t(1) << 16;
+constexpr int kGrpoCounts = 256;
+int grpo_count_blocks(int64_t slots);
+hipError_t launch_grpo(const GrpoArgs &a, uint32_t *counts, hipStream_t s);
 
 struct WgradArgs {
   const uint8_t *codes;

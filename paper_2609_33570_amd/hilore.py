@@ -70,11 +70,14 @@ def load() -> ctypes.CDLL:
     sig = {
         "hilore_status_string": (ctypes.c_char_p, [i32]),
         "hilore_version": (i32, []),
+        "hilore_grpo_coeffs_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32]),
         "hilore_grpo_coeffs": (i32, [P, P, P, P, P, i32, i32, i32, f32, f32, f32, f64,
-                                     P, P, P, P, P]),
+                                     P, P, P, P, P, ctypes.c_size_t, P]),
         "hilore_compress": (i32, [P, i32, i32, i32, P]),
         "hilore_decompress": (i32, [P, i32, i32, i32, P]),
-        "hilore_unit_exposure_risk": (i32, [P, P, i64, P, i32, f32, f32, P, P, P, P]),
+        "hilore_unit_exposure_risk_workspace_bytes": (ctypes.c_size_t, [i64, i32]),
+        "hilore_unit_exposure_risk": (i32, [P, P, i64, P, i32, f32, f32, P, P, P, P,
+                                            ctypes.c_size_t, P]),
         "hilore_dequant_wgrad": (i32, [P, P, i32, i32, P, P, i64, i64, i64, i32, P]),
         "hilore_allocate_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32]),
         "hilore_allocate": (i32, [i32, P, P, P, P, P, P, P, f64, f64, i32, i32, P, P, P, P,
@@ -176,12 +179,39 @@ def _desc_array(units: Sequence[hilore_unit_desc]):
 
 
 # ---------------------------------------------------------------- entry points --
+def _workspace(workspace, nbytes: int, stream):
+    """(pointer, size) of a caller's workspace tensor; without one, a fresh
+    device buffer of the queried size (torch's allocator) when any is needed.
+    torch reuses a freed buffer in the order of its current stream, so a call
+    on another stream must bring its own workspace."""
+    if workspace is None:
+        if nbytes == 0:
+            return None, 0, None
+        if stream is not None:
+            raise ValueError("a call on an explicit stream needs an explicit workspace")
+        import torch
+
+        workspace = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    return _p(workspace), workspace.numel() * workspace.element_size(), workspace
+
+
+def hilore_grpo_coeffs_workspace_bytes(P: int, G: int, T: int) -> int:
+    return int(load().hilore_grpo_coeffs_workspace_bytes(int(P), int(G), int(T)))
+
+
 def hilore_grpo_coeffs(rewards, logp_new, logp_old, logp_ref, mask, P, G, T, clip_eps,
-                       adv_eps, beta, n_norm, adv, ratio, flags, coeff, stream=None):
+                       adv_eps, beta, n_norm, adv, ratio, flags, coeff, workspace=None,
+                       stream=None):
+    """workspace: a device tensor of at least hilore_grpo_coeffs_workspace_bytes(P, G, T)
+    bytes, or None (a buffer of that size is then taken from torch's allocator when
+    the call counts N)."""
+    need = (hilore_grpo_coeffs_workspace_bytes(P, G, T)
+            if mask is not None and float(n_norm) <= 0.0 else 0)
+    wp, wb, _keep = _workspace(workspace, need, stream)
     st = load().hilore_grpo_coeffs(_p(rewards), _p(logp_new), _p(logp_old), _p(logp_ref),
                                    _p(mask), int(P), int(G), int(T), float(clip_eps),
                                    float(adv_eps), float(beta), float(n_norm), _p(adv),
-                                   _p(ratio), _p(flags), _p(coeff), _stream(stream))
+                                   _p(ratio), _p(flags), _p(coeff), wp, wb, _stream(stream))
     _check("hilore_grpo_coeffs", st)
 
 
@@ -197,14 +227,23 @@ def hilore_decompress(units: Sequence[hilore_unit_desc], code, block: int, strea
            load().hilore_decompress(arr, n, _code(code), int(block), _stream(stream)))
 
 
+def hilore_unit_exposure_risk_workspace_bytes(rows: int, n_units: int) -> int:
+    return int(load().hilore_unit_exposure_risk_workspace_bytes(int(rows), int(n_units)))
+
+
 def hilore_unit_exposure_risk(coeff, mask, rows: int, units: Sequence[hilore_unit_desc],
                               eps_alpha: float, eps_rel: float, exposure, risk, rel_err,
-                              stream=None):
+                              workspace=None, stream=None):
+    """workspace: a device tensor of at least
+    hilore_unit_exposure_risk_workspace_bytes(rows, len(units)) bytes, or None (a
+    buffer of that size is then taken from torch's allocator)."""
     arr, n = _desc_array(units)
+    wp, wb, _keep = _workspace(workspace, hilore_unit_exposure_risk_workspace_bytes(rows, n),
+                               stream)
     _check("hilore_unit_exposure_risk",
            load().hilore_unit_exposure_risk(_p(coeff), _p(mask), int(rows), arr, n,
                                             float(eps_alpha), float(eps_rel), _p(exposure),
-                                            _p(risk), _p(rel_err), _stream(stream)))
+                                            _p(risk), _p(rel_err), wp, wb, _stream(stream)))
 
 
 def hilore_dequant_wgrad(x_codes, x_scales, code, block: int, dy, dw, K: int, M: int, N: int,

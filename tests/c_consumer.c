@@ -29,8 +29,11 @@ int main(void) {
   expect("lora workspace, r = 0", (long)hilore_lora_grad_workspace_bytes(1024, 256, 0), 0);
 
   /* validation before any launch */
+  expect("grpo workspace, 2^18 slots", (long)hilore_grpo_coeffs_workspace_bytes(16, 16, 1024), 16);
+  expect("exposure/risk workspace, 78 units", (long)hilore_unit_exposure_risk_workspace_bytes(16384, 78),
+         78 * 8 * 32);
   expect("grpo: G = 65", hilore_grpo_coeffs(fake, fake, fake, NULL, NULL, 1, 65, 8, 0.2f, 1e-6f,
-                                            0.0f, 0.0, fake, NULL, fake, fake, NULL),
+                                            0.0f, 0.0, fake, NULL, fake, fake, NULL, 0, NULL),
          HILORE_ERR_UNSUPPORTED);
   hilore_unit_desc u;
   memset(&u, 0, sizeof u);

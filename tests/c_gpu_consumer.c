@@ -110,7 +110,7 @@ static int grpo_check(void) {
   HIP(hipMemcpy(dr, rewards, sizeof rewards, hipMemcpyHostToDevice));
   HIP(hipMemcpy(dl, lp, sizeof lp, hipMemcpyHostToDevice));
   LIB(hilore_grpo_coeffs(dr, dl, dl, NULL, NULL, P, G, T, 0.2f, 1e-6f, 0.0f, 0.0, da, dra, dfl,
-                         dco, NULL));
+                         dco, NULL, 0, NULL));
   HIP(hipDeviceSynchronize());
   HIP(hipMemcpy(adv, da, sizeof adv, hipMemcpyDeviceToHost));
   HIP(hipMemcpy(ratio, dra, sizeof ratio, hipMemcpyDeviceToHost));

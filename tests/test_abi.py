@@ -50,12 +50,12 @@ def test_status_strings_and_version(lib):
 def grpo(lib, **kw):
     a = dict(rewards=FAKE, logp_new=FAKE, logp_old=FAKE, logp_ref=None, mask=None, P=2, G=8,
              T=16, clip_eps=0.2, adv_eps=1e-6, beta=0.0, n_norm=0.0, adv=FAKE, ratio=None,
-             flags=FAKE, coeff=FAKE)
+             flags=FAKE, coeff=FAKE, ws=None, ws_bytes=0)
     a.update(kw)
     return lib.hilore_grpo_coeffs(a["rewards"], a["logp_new"], a["logp_old"], a["logp_ref"],
                                   a["mask"], a["P"], a["G"], a["T"], a["clip_eps"],
                                   a["adv_eps"], a["beta"], a["n_norm"], a["adv"], a["ratio"],
-                                  a["flags"], a["coeff"], None)
+                                  a["flags"], a["coeff"], a["ws"], a["ws_bytes"], None)
 
 
 def test_grpo_validation(lib):
@@ -73,6 +73,20 @@ def test_grpo_validation(lib):
     assert grpo(lib, flags=None) == hilore.HILORE_ERR_INVALID_ARG
     assert grpo(lib, logp_new=FAKE + 4) == hilore.HILORE_ERR_ALIGNMENT
     assert grpo(lib, mask=FAKE + 8) == hilore.HILORE_ERR_ALIGNMENT
+
+
+def test_grpo_workspace(lib):
+    """N counted over more than 2^16 slots needs the pre-pass workspace: 4 bytes
+    per 2^16 slots, at most 1 KB; nothing for smaller calls or a given N."""
+    f = lib.hilore_grpo_coeffs_workspace_bytes
+    assert f(1, 8, 2048) == 0 and f(2, 16, 2048) == 0          # 16384 and 65536 slots
+    assert f(2, 16, 2049) == 2 * 4                             # just above 2^16
+    assert f(2, 16, 1 << 21) == 256 * 4 and f(64, 64, 1 << 18) == 256 * 4
+    assert f(-1, 8, 16) == 0 and f(1, 0, 16) == 0
+    big = dict(P=16, G=16, T=1024, mask=FAKE)                  # 2^18 slots
+    assert grpo(lib, **big) == hilore.HILORE_ERR_INVALID_ARG   # no workspace
+    assert grpo(lib, ws=FAKE, ws_bytes=15, **big) == hilore.HILORE_ERR_WORKSPACE
+    assert grpo(lib, ws=FAKE + 4, ws_bytes=16, **big) == hilore.HILORE_ERR_ALIGNMENT
     assert grpo(lib, P=0) == hilore.HILORE_OK  # nothing to do, nothing launched
 
 
@@ -131,10 +145,11 @@ def test_decompress_specific_validation(lib):
     assert codec(lib, "hilore_decompress", [unit(xhat=None)]) == hilore.HILORE_ERR_INVALID_ARG
 
 
-def risk(lib, units, rows=4, coeff=FAKE, mask=None, outs=(FAKE, FAKE, FAKE), eps=(1e-8, 1e-8)):
+def risk(lib, units, rows=4, coeff=FAKE, mask=None, outs=(FAKE, FAKE, FAKE), eps=(1e-8, 1e-8),
+         ws=FAKE, ws_bytes=1 << 20):
     arr = (hilore.hilore_unit_desc * max(1, len(units)))(*units)
     return lib.hilore_unit_exposure_risk(coeff, mask, rows, arr, len(units), eps[0], eps[1],
-                                         outs[0], outs[1], outs[2], None)
+                                         outs[0], outs[1], outs[2], ws, ws_bytes, None)
 
 
 def test_exposure_risk_validation(lib):
@@ -149,6 +164,21 @@ def test_exposure_risk_validation(lib):
     assert risk(lib, [ok], eps=(-1.0, 1e-8)) == E.HILORE_ERR_INVALID_ARG
     assert risk(lib, [unit(row_ss_x=FAKE, row_ss_err=FAKE, cols=0)]) == E.HILORE_ERR_INVALID_ARG
     assert risk(lib, []) == E.HILORE_OK
+    assert risk(lib, [ok], ws=None) == E.HILORE_ERR_INVALID_ARG
+    assert risk(lib, [ok], ws=FAKE + 8) == E.HILORE_ERR_ALIGNMENT
+    assert risk(lib, [ok], ws_bytes=31) == E.HILORE_ERR_WORKSPACE
+    big = unit(row_ss_x=FAKE, row_ss_err=FAKE, rows=1 << 24)
+    assert risk(lib, [big], rows=1 << 24) == E.HILORE_ERR_UNSUPPORTED
+
+
+def test_exposure_risk_workspace_size(lib):
+    """32 bytes per unit per chunk of 2048 rows; nothing without rows."""
+    f = lib.hilore_unit_exposure_risk_workspace_bytes
+    assert f(16384, 2) == 2 * 8 * 32
+    assert f(16384, 78) == 78 * 8 * 32
+    assert f(2049, 3) == 3 * 2 * 32
+    assert f(1, 1) == 32 and f(0, 5) == 0 and f(100, 0) == 0
+    assert f(-1, 1) == 0 and f(1 << 24, 1) == 0
 
 
 def wgrad(lib, **kw):

@@ -1,7 +1,7 @@
 """The hot path captured in a HIP graph (through torch.cuda.graph): the calls
-allocate nothing, record no memset and never synchronise the host, so one
-step (coefficients, compress with row sums, exposure and risk, decompress,
-the fused wgrad) captures as is.  The graph is replayed three times with new
+allocate nothing (the exposure/risk workspace is the caller's), record no
+memset and never synchronise the host, so one step (coefficients, compress
+with row sums, exposure and risk, decompress, the fused wgrad) captures as is.  The graph is replayed three times with new
 inputs written eagerly in between, and every replay must equal the same step
 run eagerly on the same inputs, bit for bit."""
 import numpy as np
@@ -35,7 +35,9 @@ def buffers(hl):
          "wc": torch.empty((K, M), dtype=torch.uint8, device="cuda"),
          "ws": torch.empty((K, M // BLOCK), device="cuda"),
          "dy": torch.empty((K, N), dtype=torch.bfloat16, device="cuda"),
-         "dw": torch.empty((M, N), device="cuda")}
+         "dw": torch.empty((M, N), device="cuda"),
+         "risk_ws": torch.empty(hl.hilore_unit_exposure_risk_workspace_bytes(ROWS, 1),
+                                dtype=torch.uint8, device="cuda")}
     b["unit"] = hl.unit_desc(x=b["x"], codes=b["codes"], scales=b["scales"], xhat=b["xhat"],
                              row_ss_x=b["ssx"], row_ss_err=b["sse"])
     return b
@@ -59,7 +61,7 @@ def step(hl, b):
                           0.0, 0.0, b["adv"], b["ratio"], b["flags"], b["coeff"])
     hl.hilore_compress([b["unit"]], CODE, BLOCK)
     hl.hilore_unit_exposure_risk(b["coeff"], None, ROWS, [b["unit"]], 1e-8, 1e-8, b["expo"],
-                                 b["risk"], b["rel"])
+                                 b["risk"], b["rel"], workspace=b["risk_ws"])
     hl.hilore_decompress([b["unit"]], CODE, BLOCK)
     hl.hilore_dequant_wgrad(b["wc"], b["ws"], CODE, BLOCK, b["dy"], b["dw"], K, M, N)
 

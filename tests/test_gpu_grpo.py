@@ -107,3 +107,58 @@ def test_deterministic(hl, orc):
     r2 = run_gpu(hl, b, beta=1e-3)
     for a1, a2 in zip(r1, r2):
         assert_bytes_equal(a1, a2, "repeat")
+
+
+@pytest.mark.parametrize("P,G,T", [(3, 7, 4099), (64, 16, 1024)])
+def test_counted_by_prepass(hl, orc, P, G, T):
+    """More than 2^16 slots with N counted: a count pre-pass writes one count per
+    2^16 slots into the workspace and the coefficient launch adds them.
+    3 x 7 x 4099 = 86079 slots: two counting workgroups and a byte tail of 15;
+    2^20 slots: 16 of them."""
+    b = wl.grpo_batch(P, G, T, seed=P * 100 + T, delta_sigma=0.2, pad_frac=0.3)
+    assert hl.hilore_grpo_coeffs_workspace_bytes(P, G, T) == 4 * -(-(P * G * T) // 65536)
+    check(hl, orc, b)
+
+
+def test_mask_bytes_other_than_one(hl, orc):
+    """Any nonzero mask byte is a valid slot, in the in-kernel count and in the
+    pre-pass."""
+    for P, G, T in ((2, 8, 1024), (8, 16, 1024)):
+        b = wl.grpo_batch(P, G, T, seed=38 + P, pad_frac=0.3)
+        g = np.random.default_rng(P)
+        vals = g.choice(np.array([1, 2, 128, 255], np.uint8), b.mask.size)
+        b.mask = (b.mask * vals).astype(np.uint8)
+        check(hl, orc, b)
+
+
+def test_counted_2p22_slots_linear(hl, orc):
+    """2^22 masked slots with N counted (the pre-pass path), against the oracle,
+    and timed: a count that every workgroup repeated over the whole mask would
+    read 4 MB per workgroup (16 GB per call); the pre-pass reads it once more,
+    so a call stays far below a millisecond."""
+    P, G, T = 128, 16, 2048
+    b = wl.grpo_batch(P, G, T, seed=39, pad_frac=0.3)
+    check(hl, orc, b)
+    n = P * G * T
+    rew, ln, lo, m = dev(b.rewards), dev(b.logp_new), dev(b.logp_old), dev(b.mask)
+    adv = torch.empty(P * G, device="cuda")
+    flags = torch.empty(n, dtype=torch.uint8, device="cuda")
+    coeff = torch.empty(n, device="cuda")
+    ratio = torch.empty(n, device="cuda")
+    ws = torch.empty(hl.hilore_grpo_coeffs_workspace_bytes(P, G, T), dtype=torch.uint8,
+                     device="cuda")
+
+    def call():
+        hl.hilore_grpo_coeffs(rew, ln, lo, None, m, P, G, T, 0.2, 1e-6, 0.0, 0.0, adv, ratio,
+                              flags, coeff, workspace=ws)
+
+    call()
+    e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+    torch.cuda.synchronize()
+    e0.record()
+    for _ in range(10):
+        call()
+    e1.record()
+    torch.cuda.synchronize()
+    ms = e0.elapsed_time(e1) / 10
+    assert ms < 0.5, f"{ms:.3f} ms per call on 2^22 slots"

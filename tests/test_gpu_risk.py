@@ -90,3 +90,75 @@ def test_deterministic(hl, orc):
     second = gpu_pipeline(hl, b, xs, 1, 128)
     for name, a1, a2 in zip(["exposure", "risk", "rel_err"], first, second):
         assert np.array_equal(a1.view(np.uint32), a2.view(np.uint32)), name
+
+
+def risk_on(hl, orc, coeff, mask, xs, code, block, workspace=None):
+    """GPU: compress with row sums, then the reduction on the given coefficients;
+    oracle: the same from its own codec, in fp64."""
+    rows = coeff.size
+    units, keep = [], []
+    for x in xs:
+        xd = dev(x)
+        codes = torch.empty(x.shape, dtype=torch.uint8, device="cuda")
+        scales = torch.empty((x.shape[0], x.shape[1] // block), dtype=torch.float32, device="cuda")
+        ssx = filled(rows, torch.float32, float("nan"))
+        sse = filled(rows, torch.float32, float("nan"))
+        keep.append((xd, codes, scales, ssx, sse))
+        units.append(hl.unit_desc(x=xd, codes=codes, scales=scales, row_ss_x=ssx, row_ss_err=sse))
+    hl.hilore_compress(units, code, block)
+    k = len(xs)
+    outs = [filled(k, torch.float32, float("nan")) for _ in range(3)]
+    m = dev(mask) if mask is not None else None
+    hl.hilore_unit_exposure_risk(dev(coeff), m, rows, units, 1e-8, 1e-8, *outs,
+                                 workspace=workspace)
+    torch.cuda.synchronize()
+    want = []
+    for x in xs:
+        c, s = orc.quantize(x, code, block)
+        ss_x, ss_e = orc.row_stats(x, orc.dequantize(c, s, code, block))
+        want.append(orc.unit_exposure_risk(coeff.astype(np.float64), mask, ss_x, ss_e, x.shape[1]))
+    return [host(o) for o in outs], [np.array(v) for v in zip(*want)]
+
+
+def random_coeff(rows, seed, pad=0.3):
+    g = np.random.default_rng(seed)
+    mask = (g.random(rows) >= pad).astype(np.uint8)
+    coeff = (g.normal(0.0, 1e-4, rows) * mask).astype(np.float32)
+    return coeff, mask
+
+
+@pytest.mark.parametrize("rows", [1, 3, 2048, 2049, 7171], ids=lambda r: f"rows{r}")
+def test_ragged_row_counts(hl, orc, rows):
+    """Chunks of 2048 rows read as runs of 4: one and three rows (tail only), a
+    whole chunk, one past it, and 3 chunks plus a tail of 1027 rows."""
+    coeff, mask = random_coeff(rows, 700 + rows)
+    xs = [wl.activation_host(rows, c, seed=710 + i, outliers=("channels", 0.005, 30.0))
+          for i, c in enumerate([128, 384])]
+    got, want = risk_on(hl, orc, coeff, mask, xs, 1, 128)
+    for name, gv, ov in zip(["exposure", "risk", "rel_err"], got, want):
+        assert_close(gv, ov, f"{name} rows={rows}")
+
+
+def test_more_units_than_one_launch(hl, orc):
+    """100 units: two partial launches (96 units travel in one launch's
+    arguments) and one fold; an explicit workspace of exactly the queried size."""
+    rows = 2100
+    coeff, mask = random_coeff(rows, 720)
+    xs = [wl.activation_host(rows, 64 * (1 + i % 3), seed=730 + i) for i in range(100)]
+    nbytes = hl.hilore_unit_exposure_risk_workspace_bytes(rows, len(xs))
+    assert nbytes == 100 * 2 * 32
+    ws = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+    got, want = risk_on(hl, orc, coeff, mask, xs, 0, 64, workspace=ws)
+    for name, gv, ov in zip(["exposure", "risk", "rel_err"], got, want):
+        assert_close(gv, ov, name)
+
+
+def test_no_rows(hl):
+    """rows = 0: nothing to read and no workspace; exposure and risk 0, rel_err
+    0 / (0 + eps) = 0."""
+    outs = [filled(2, torch.float32, float("nan")) for _ in range(3)]
+    d = [hl.unit_desc(rows=0, cols=128), hl.unit_desc(rows=0, cols=64)]
+    hl.hilore_unit_exposure_risk(None, None, 0, d, 1e-8, 1e-8, *outs)
+    torch.cuda.synchronize()
+    for o in outs:
+        assert (host(o) == 0).all()
