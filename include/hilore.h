@@ -22,8 +22,9 @@
  * Conventions shared by every entry point:
  *   - Every tensor pointer is a DEVICE pointer owned by the caller.  The
  *     library never allocates, frees or retains memory, and keeps no state
- *     between calls.  hilore_unit_desc arrays are HOST memory, read during the
- *     call only.
+ *     between calls (the one exception, hilore_unit_exposure_risk_noalloc,
+ *     uses a fixed device array of its own).  hilore_unit_desc arrays are
+ *     HOST memory, read during the call only.
  *   - `stream` is a hipStream_t passed as void* (NULL = the default stream).
  *     All work is enqueued on it without a host synchronisation; outputs are
  *     valid once the stream reaches them.
@@ -213,6 +214,27 @@ hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask,
                                         float eps_alpha, float eps_rel, float *exposure,
                                         float *risk, float *rel_err, void *workspace,
                                         size_t workspace_bytes, void *stream);
+
+/*
+ * hilore_unit_exposure_risk without a workspace, for callers that cannot
+ * allocate device memory or pass a buffer for it: code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation.  Same
+ * arguments (less the workspace), kernels and results, bit for bit.  The
+ * partial sums live in a fixed 1 MiB array in device memory that the library
+ * holds on every GPU it runs on until the process ends (its address is looked
+ * up once per device, on the first call made with that device current); the
+ * call allocates nothing.  One call needs 32 bytes per unit per 2048 rows, so
+ * units * ceil(rows / 2048) may be at most 32768 (78 units of 16384 rows use
+ * 624), else the call returns WORKSPACE and enqueues nothing.  Every call on
+ * one GPU shares that array: calls that overlap on one GPU (other streams,
+ * other threads) race and give wrong results; calls in stream order do not.
+ * Nothing in the array needs to start at zero.
+ */
+hilore_status hilore_unit_exposure_risk_noalloc(const float *coeff, const uint8_t *mask,
+                                                int64_t rows, const hilore_unit_desc *units,
+                                                int n_units, float eps_alpha, float eps_rel,
+                                                float *exposure, float *risk, float *rel_err,
+                                                void *stream);
 
 /*
  * Weight gradient of a linear layer whose saved input is an L unit, with the

@@ -308,6 +308,21 @@ hilore_status hilore_unit_exposure_risk(const float *coeff, const uint8_t *mask,
                            static_cast<hipStream_t>(stream));
 }
 
+hilore_status hilore_unit_exposure_risk_noalloc(const float *coeff, const uint8_t *mask,
+                                                int64_t rows, const hilore_unit_desc *units,
+                                                int n_units, float eps_alpha, float eps_rel,
+                                                float *exposure, float *risk, float *rel_err,
+                                                void *stream) {
+  const hilore_status st = check_exposure_risk(coeff, mask, rows, units, n_units, eps_alpha,
+                                               eps_rel, exposure, risk, rel_err);
+  if (st != HILORE_OK || n_units == 0) return st;
+  if (risk_workspace_bytes(rows, n_units) > hilore::kRiskScratchBytes) return HILORE_ERR_WORKSPACE;
+  float *part = nullptr;
+  if (hilore::risk_scratch(&part) != hipSuccess) return HILORE_ERR_HIP;
+  return run_exposure_risk(coeff, mask, rows, units, n_units, eps_alpha, eps_rel, exposure, risk,
+                           rel_err, part, static_cast<hipStream_t>(stream));
+}
+
 hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, int code,
                                    int block, const uint16_t *dy, float *dw, int64_t K,
                                    int64_t M, int64_t N, int accumulate, void *stream) {

@@ -82,6 +82,10 @@ hipError_t launch_risk_partial(const RiskBatch &b, hipStream_t s);
 hipError_t launch_risk_fold(const float *part, int n_units, int64_t n_chunks, float eps_alpha,
                             float eps_rel, float *exposure, float *risk, float *rel_err,
                             hipStream_t s);
+// The allocation-free variant keeps its partials in a fixed device array of
+// this many bytes; risk_scratch gives its address on the current device.
+constexpr size_t kRiskScratchBytes = size_t(1) << 20;
+hipError_t risk_scratch(float **ptr);
 
 struct GrpoArgs {
   const float *rewards, *logp_new, *logp_old, *logp_ref;

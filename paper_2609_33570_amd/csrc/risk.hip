@@ -24,6 +24,8 @@
 // unit adds its chunk partials (lane l takes chunks l, l + 64, ... in order,
 // then a butterfly) and forms the three outputs.  Every order is fixed, so the
 // results depend on nothing but the inputs; no floating-point atomics.
+#include <mutex>
+
 #include "device_common.hpp"
 #include "hilore_internal.hpp"
 
@@ -153,6 +155,12 @@ __global__ __launch_bounds__(kWave) void risk_fold_kernel(const float *part, int
   }
 }
 
+// Fixed device scratch of the allocation-free variant: the partials of one
+// call.  Every GPU the library runs on holds its own copy until the process
+// ends; host code never uses this name as an address, only what
+// hipGetSymbolAddress returns for the current device (risk_scratch below).
+__device__ __align__(256) float scratch[kRiskScratchBytes / sizeof(float)];
+
 }  // namespace
 
 int64_t risk_chunks(int64_t rows) { return (rows + kRiskChunkRows - 1) / kRiskChunkRows; }
@@ -171,6 +179,26 @@ hipError_t launch_risk_fold(const float *part, int n_units, int64_t n_chunks, fl
   hipLaunchKernelGGL(risk_fold_kernel, dim3((unsigned)n_units), dim3(kWave), 0, s, part, n_chunks,
                      eps_alpha, eps_rel, exposure, risk, rel_err);
   return hipGetLastError();
+}
+
+hipError_t risk_scratch(float **ptr) {
+  constexpr int kMaxDevices = 64;
+  static std::once_flag once[kMaxDevices];
+  static float *addr[kMaxDevices];
+  static hipError_t err[kMaxDevices];
+  int dev = 0;
+  const hipError_t e = hipGetDevice(&dev);
+  if (e != hipSuccess) return e;
+  if (dev < 0 || dev >= kMaxDevices) return hipErrorInvalidDevice;
+  // once per device, on the first call made with that device current
+  std::call_once(once[dev], [dev]() {
+    void *p = nullptr;
+    err[dev] = hipGetSymbolAddress(&p, HIP_SYMBOL(scratch));
+    addr[dev] = err[dev] == hipSuccess ? static_cast<float *>(p) : nullptr;
+  });
+  if (err[dev] != hipSuccess) return err[dev];
+  *ptr = addr[dev];
+  return hipSuccess;
 }
 
 }  // namespace hilore

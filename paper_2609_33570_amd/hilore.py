@@ -78,6 +78,7 @@ def load() -> ctypes.CDLL:
         "hilore_unit_exposure_risk_workspace_bytes": (ctypes.c_size_t, [i64, i32]),
         "hilore_unit_exposure_risk": (i32, [P, P, i64, P, i32, f32, f32, P, P, P, P,
                                             ctypes.c_size_t, P]),
+        "hilore_unit_exposure_risk_noalloc": (i32, [P, P, i64, P, i32, f32, f32, P, P, P, P]),
         "hilore_dequant_wgrad": (i32, [P, P, i32, i32, P, P, i64, i64, i64, i32, P]),
         "hilore_allocate_workspace_bytes": (ctypes.c_size_t, [i32, i32, i32]),
         "hilore_allocate": (i32, [i32, P, P, P, P, P, P, P, f64, f64, i32, i32, P, P, P, P,
@@ -244,6 +245,19 @@ def hilore_unit_exposure_risk(coeff, mask, rows: int, units: Sequence[hilore_uni
            load().hilore_unit_exposure_risk(_p(coeff), _p(mask), int(rows), arr, n,
                                             float(eps_alpha), float(eps_rel), _p(exposure),
                                             _p(risk), _p(rel_err), wp, wb, _stream(stream)))
+
+
+def hilore_unit_exposure_risk_noalloc(coeff, mask, rows: int, units: Sequence[hilore_unit_desc],
+                                      eps_alpha: float, eps_rel: float, exposure, risk, rel_err,
+                                      stream=None):
+    """hilore_unit_exposure_risk with its partials in the library's fixed device
+    array (no workspace): for callers that cannot allocate."""
+    arr, n = _desc_array(units)
+    _check("hilore_unit_exposure_risk_noalloc",
+           load().hilore_unit_exposure_risk_noalloc(_p(coeff), _p(mask), int(rows), arr, n,
+                                                    float(eps_alpha), float(eps_rel),
+                                                    _p(exposure), _p(risk), _p(rel_err),
+                                                    _stream(stream)))
 
 
 def hilore_dequant_wgrad(x_codes, x_scales, code, block: int, dy, dw, K: int, M: int, N: int,
