@@ -182,9 +182,9 @@ def _desc_array(units: Sequence[hilore_unit_desc]):
 # ---------------------------------------------------------------- entry points --
 def _workspace(workspace, nbytes: int, stream):
     """(pointer, size) of a caller's workspace tensor; without one, a fresh
-    device buffer of the queried size (torch's allocator) when any is needed.
-    torch reuses a freed buffer in the order of its current stream, so a call
-    on another stream must bring its own workspace."""
+    zeroed device buffer of the queried size (torch's allocator) when any is
+    needed.  torch reuses a freed buffer in the order of its current stream, so
+    a call on another stream must bring its own workspace."""
     if workspace is None:
         if nbytes == 0:
             return None, 0, None
@@ -192,7 +192,7 @@ def _workspace(workspace, nbytes: int, stream):
             raise ValueError("a call on an explicit stream needs an explicit workspace")
         import torch
 
-        workspace = torch.empty(nbytes, dtype=torch.uint8, device="cuda")
+        workspace = torch.zeros(nbytes, dtype=torch.uint8, device="cuda")
     return _p(workspace), workspace.numel() * workspace.element_size(), workspace
 
 

@@ -91,6 +91,30 @@ def grpo_batch(P: int, G: int, T: int, seed: int, delta_sigma: float = 0.05,
     return GrpoBatch(P, G, T, rewards, new, old, ref, mask)
 
 
+def grpo_batch_device(P: int, G: int, T: int, seed: int, delta_sigma: float = 0.05,
+                      pad_frac: Optional[float] = None, device="cuda"):
+    """Device-side GRPO inputs with grpo_batch's recipe (Bernoulli(0.5) rewards,
+    s_old ~ N(-2, 0.5), s_new = s_old + N(0, delta_sigma), trailing padding of
+    a fraction pad_frac drawn by pad_lengths), drawn with torch's generator in
+    fp32 for batches too large to draw on the host.  Returns (rewards,
+    logp_new, logp_old, mask or None) as device tensors; the values differ from
+    grpo_batch's for the same seed."""
+    import torch
+
+    R = P * G
+    gen = torch.Generator(device=device)
+    gen.manual_seed(int(seed))
+    rewards = (torch.rand(R, generator=gen, device=device) < 0.5).to(torch.float32)
+    old = torch.randn(R * T, generator=gen, device=device).mul_(0.5).sub_(2.0)
+    new = torch.randn(R * T, generator=gen, device=device).mul_(delta_sigma).add_(old)
+    mask = None
+    if pad_frac is not None:
+        pad = torch.from_numpy(pad_lengths(R, T, pad_frac, rng(seed, 1))).to(device)
+        t = torch.arange(T, device=device)
+        mask = (t[None, :] < (T - pad)[:, None]).to(torch.uint8).reshape(-1)
+    return rewards, new, old, mask
+
+
 # -------------------------------------------------------------- activations --
 def activation_host(rows: int, cols: int, seed: int, dist: str = "normal",
                     outliers: Optional[Tuple[str, float, float]] = None,
