@@ -1,10 +1,16 @@
 """Helpers shared by the GPU parity tests: host <-> device copies and the
 tolerance rule.
 
-Tolerance for floating-point outputs (coefficients, ratios, row sums,
-exposure, risk, relative error): |gpu - truth| <= 1e-5 * max(|truth|, 1e-3 *
-max|truth|), truth in fp64 from the oracle.  Bit-exact outputs (advantages,
-flags, codes, scales, reconstructions) are compared as raw bytes.
+Tolerance for floating-point outputs: |gpu - truth| <= 1e-5 * |truth|
+(truth in fp64 from the oracle) where nothing cancels: ratios, and update
+coefficients without the KL term (each a single product of rounded factors).
+Where terms of opposite sign can cancel (coefficients with the K3 KL term,
+whose policy and KL parts may nearly annul) or an fp32 sum is compared with
+its fp64 value (row sums, exposure, risk, relative error), the absolute error
+is bounded instead by 1e-5 * max(|truth|, 1e-3 * max|truth|): an element far
+below the largest carries the rounding of the terms it was formed from, not
+its own.  Bit-exact outputs (advantages, flags, codes, scales,
+reconstructions) are compared as raw bytes.
 """
 import numpy as np
 import torch
@@ -43,13 +49,14 @@ def filled(shape, dtype, value=0) -> torch.Tensor:
     return torch.full(shape, value, dtype=dtype, device="cuda")
 
 
-def assert_close(gpu, truth, what="", rel=REL_TOL):
+def assert_close(gpu, truth, what="", rel=REL_TOL, floor_frac=1e-3):
+    """floor_frac = 0: a pure relative check (see the module docstring)."""
     gpu = np.asarray(gpu, dtype=np.float64)
     truth = np.asarray(truth, dtype=np.float64)
     assert gpu.shape == truth.shape, what
     if truth.size == 0:
         return
-    floor = 1e-3 * np.abs(truth).max()
+    floor = floor_frac * np.abs(truth).max()
     err = np.abs(gpu - truth)
     lim = rel * np.maximum(np.abs(truth), floor)
     bad = err > lim

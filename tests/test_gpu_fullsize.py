@@ -4,12 +4,14 @@ rows / entries elsewhere.
 
   - Qwen2-7B-width layer: hidden 16384x3584 and MLP 16384x18944, fp8-e4m3
     1x128 (the hidden unit fully, the MLP unit on sampled rows);
-  - whole-model plan: 78 L units of 16384x3584, int8 1x64, one batched call;
+  - whole-model plan: 78 L units of 16384x3584, int8 1x64, one batched call
+    (sampled rows of every unit, one whole unit of every compress launch);
   - fused wgrad: X 16384x4096 fp8-e4m3 1x128, dY 16384x4096, dW 4096x4096
     (the 512x512 corner against fp64, sampled entries, and the whole matrix
     against an fp32 GEMM on the decompressed operand);
   - Llama-3-8B-shaped stress: 32 MLP intermediates 32768x14336, Student-t,
-    int8 1x128 (sampled rows of every unit).
+    int8 1x128, with its 30%-padded GRPO batch end to end (two whole units,
+    sampled rows of the others, every unit's exposure/risk).
 The inputs are drawn on the device (torch's generator), then the rows the
 oracle needs are copied back, byte for byte.
 """
@@ -58,6 +60,28 @@ def check_rows(orc, u, idx, code, block, what):
         o_ssx, o_sse = orc.row_stats(x, o_xhat)
         assert_close(host(u["ssx"])[idx], o_ssx, what + " ss_x")
         assert_close(host(u["sse"])[idx], o_sse, what + " ss_err")
+
+
+def check_unit(orc, u, code, block, what, chunk=4096):
+    """Every row of a unit against the oracle, in chunks of rows (codes, scales
+    and the reconstruction byte for byte, the row sums to tolerance); returns
+    the oracle's fp64 row sums."""
+    rows = u["x"].shape[0]
+    ss = []
+    for r0 in range(0, rows, chunk):
+        r1 = min(rows, r0 + chunk)
+        x = host(u["x"][r0:r1])
+        o_codes, o_scales = orc.quantize(x, code, block)
+        o_xhat = orc.dequantize(o_codes, o_scales, code, block)
+        assert_bytes_equal(host(u["codes"][r0:r1]), o_codes, f"{what} codes rows {r0}..")
+        assert_bytes_equal(host(u["scales"][r0:r1]), o_scales, f"{what} scales rows {r0}..")
+        assert_bytes_equal(host(u["xhat"][r0:r1]), o_xhat, f"{what} xhat rows {r0}..")
+        o_ssx, o_sse = orc.row_stats(x, o_xhat)
+        ss.append((o_ssx, o_sse))
+        if u["ssx"] is not None:
+            assert_close(host(u["ssx"][r0:r1]), o_ssx, f"{what} ss_x rows {r0}..")
+            assert_close(host(u["sse"][r0:r1]), o_sse, f"{what} ss_err rows {r0}..")
+    return np.concatenate([a for a, _ in ss]), np.concatenate([b for _, b in ss])
 
 
 def grpo_on_gpu(hl, b):
@@ -141,17 +165,22 @@ def test_qwen2_7b_plan(hl, orc):
     g = np.random.default_rng(2)
     for i, u in enumerate(units):
         check_rows(orc, u, np.sort(g.choice(rows, 6, replace=False)), code, block, f"unit {i}")
+    # the batched call encodes 16 units per launch: one whole unit of every launch
+    for i in range(0, n, 16):
+        check_unit(orc, units[i], code, block, f"unit {i} (launch {i // 16})")
     ge, gk, gr = host(expo), host(risk), host(rel)
     for i in (0, n - 1):  # two units end to end against the oracle
         x = host(units[i]["x"])
         c, s = orc.quantize(x, code, block)
         ssx, sse = orc.row_stats(x, orc.dequantize(c, s, code, block))
         e, k, r = orc.unit_exposure_risk(o_coeff, None, ssx, sse, 3584)
-        assert_close([ge[i], gk[i], gr[i]], [e, k, r], f"unit {i} exposure/risk/rel")
+        for name, gv, ov in (("exposure", ge[i], e), ("risk", gk[i], k), ("rel_err", gr[i], r)):
+            assert_close([gv], [ov], f"unit {i} {name}")
     for i in range(n):  # every unit's reduction from its GPU row sums
         e, k, r = orc.unit_exposure_risk(o_coeff, None, host(units[i]["ssx"]).astype(np.float64),
                                          host(units[i]["sse"]).astype(np.float64), 3584)
-        assert_close([ge[i], gk[i], gr[i]], [e, k, r], f"unit {i} reduction")
+        for name, gv, ov in (("exposure", ge[i], e), ("risk", gk[i], k), ("rel_err", gr[i], r)):
+            assert_close([gv], [ov], f"unit {i} {name} (from its GPU row sums)")
     assert np.isfinite(gk.astype(np.float64).sum())
 
 
@@ -192,16 +221,59 @@ def test_wgrad_4096(hl, orc):
 
 
 def test_llama3_8b_stress(hl, orc):
+    """The stress workload end to end as the benchmark runs it: coefficients of
+    the 30%-padded GRPO batch (N counted in the launch), one batched compress
+    with row sums of the 32 units, exposure/risk under the length mask, one
+    batched decompress.  Checked: flags and advantages bit for bit and the
+    coefficients to tolerance; two whole units (one of each 16-unit launch)
+    row for row against the oracle, sampled rows of every other unit; every
+    unit's exposure/risk/rel_err from its GPU row sums in fp64, and for the
+    two whole units from the oracle's own row sums."""
     w = wl.LLAMA3_8B_STRESS
     code, block = 0, 128
+    b = wl.grpo_batch(w.P, w.G, w.T, seed=w.seed, pad_frac=w.pad_frac)
+    rows = b.P * b.G * b.T
+    assert rows == w.units[0].rows
+    R = b.P * b.G
+    adv = filled(R, torch.float32, float("nan"))
+    flags = filled(rows, torch.uint8, 0xEE)
+    coeff = filled(rows, torch.float32, float("nan"))
+    m = dev(b.mask)
+    hl.hilore_grpo_coeffs(dev(b.rewards), dev(b.logp_new), dev(b.logp_old), None, m, b.P, b.G,
+                          b.T, 0.2, 1e-6, 0.0, 0.0, adv, None, flags, coeff)
     units = []
-    for i, s in enumerate(w.units):
-        units.append(alloc_unit(hl, wl.activation_device(s.rows, s.cols, w.seed * 100 + i,
+    for i, sh in enumerate(w.units):
+        units.append(alloc_unit(hl, wl.activation_device(sh.rows, sh.cols, w.seed * 100 + i,
                                                          dist="student_t3"), block))
+    n = len(units)
     hl.hilore_compress([u["dc"] for u in units], code, block)
+    expo = filled(n, torch.float32, float("nan"))
+    risk = filled(n, torch.float32, float("nan"))
+    rel = filled(n, torch.float32, float("nan"))
+    hl.hilore_unit_exposure_risk(coeff, m, rows, [u["dc"] for u in units], 1e-8, 1e-8, expo,
+                                 risk, rel)
     hl.hilore_decompress([u["dd"] for u in units], code, block)
     torch.cuda.synchronize()
+    o_adv, _, o_flags, o_coeff = orc.grpo_coeffs(b.rewards, b.logp_new, b.logp_old, None, b.mask,
+                                                 b.P, b.G, b.T)
+    assert_bytes_equal(host(adv), o_adv, "advantages")
+    assert_bytes_equal(host(flags), o_flags, "flags")
+    assert_close(host(coeff), o_coeff, "coefficients", floor_frac=0.0)
+    assert abs(1.0 - b.mask.mean() - w.pad_frac) < 1e-4
+    ge, gk, gr = host(expo), host(risk), host(rel)
     g = np.random.default_rng(5)
+    whole = (0, 16)
     for i, u in enumerate(units):
-        check_rows(orc, u, np.sort(g.choice(w.units[0].rows, 3, replace=False)), code, block,
-                   f"layer {i}")
+        if i in whole:
+            ssx, sse = check_unit(orc, u, code, block, f"layer {i}")
+            e, k, r = orc.unit_exposure_risk(o_coeff, b.mask, ssx, sse, w.units[0].cols)
+            for name, gv, ov in (("exposure", ge[i], e), ("risk", gk[i], k), ("rel_err", gr[i], r)):
+                assert_close([gv], [ov], f"layer {i} {name}")
+        else:
+            check_rows(orc, u, np.sort(g.choice(rows, 3, replace=False)), code, block,
+                       f"layer {i}")
+        e, k, r = orc.unit_exposure_risk(o_coeff, b.mask, host(u["ssx"]).astype(np.float64),
+                                         host(u["sse"]).astype(np.float64), w.units[0].cols)
+        for name, gv, ov in (("exposure", ge[i], e), ("risk", gk[i], k), ("rel_err", gr[i], r)):
+            assert_close([gv], [ov], f"layer {i} {name} (from its GPU row sums)")
+    assert (ge > 0).all() and (gk > 0).all() and (gr > 0).all()
