@@ -269,11 +269,14 @@ hilore_status hilore_dequant_wgrad(const void *x_codes, const float *x_scales, i
  *   scale    the adapter scaling alpha / r (applied to the fp32 sum; exact for powers of 2)
  *   accumulate: 0 overwrites da, 1 adds to it
  * bf16 x bf16 products, fp32 accumulation (MFMA), xhat never written to memory;
- * each code is read once per 16 adapter rows.  Partial sums over token ranges
- * go to `workspace` and are added in a fixed order (no floating-point atomics).
+ * each code is read once per pass of up to 80 adapter rows, so adapters that
+ * share one input (q/k/v, gate/up) are best passed side by side in dh (r = 48,
+ * 80).  Partial sums over token ranges go to `workspace` and are added in a
+ * fixed order (no floating-point atomics).
  * workspace: device memory of at least hilore_lora_grad_workspace_bytes(K, M, r)
- * bytes (8 MB below M = 65536 columns), 16-byte aligned,
- * contents on entry irrelevant; calls sharing it must not overlap.
+ * bytes (below M = 65536 columns: 8 MB per 16 adapter rows of the widest
+ * pass, so at most 40 MB), 16-byte aligned, contents on entry irrelevant;
+ * calls sharing it must not overlap.
  * With HILORE_CODE_FP8_E4M3FN_CAST (block = 0, x_scales unused) xhat = value(code).
  * Limits: M % block == 0, M % 16 == 0, M < 2^26, K < 2^31, r even, 2 <= r <= 4096.
  * Errors: negative sizes, r < 1, non-finite scale, null pointers -> INVALID_ARG;

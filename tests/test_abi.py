@@ -302,9 +302,13 @@ def test_calibration_entry_points_validate(lib):
 def test_lora_grad_validation(lib):
     E = hilore
     ws = lib.hilore_lora_grad_workspace_bytes
-    # 256 workgroups x 2 partial [16][256] fp32 slots (a range meets at most two strips)
+    # 256 workgroups x 2 partial [16 R][256] fp32 slots (a range meets at most two
+    # strips), R = row blocks of 16 in the widest pass (passes of up to 80 rows)
     assert ws(16384, 18944, 16) == 256 * 2 * 16 * 256 * 4
-    assert ws(16384, 18944, 64) == ws(16384, 18944, 16)  # passes reuse the slots
+    assert ws(16384, 18944, 64) == 4 * ws(16384, 18944, 16)
+    assert ws(16384, 18944, 80) == 5 * ws(16384, 18944, 16)
+    assert ws(16384, 18944, 96) == ws(16384, 18944, 80)  # later passes reuse the slots
+    assert ws(16384, 18944, 18) == 2 * ws(16384, 18944, 16)
     assert ws(32, 256, 16) == 1 * 2 * 16 * 256 * 4       # one k-step: one workgroup
     assert ws(-1, 256, 16) == 0 and ws(32, 256, 0) == 0
     big = 1 << 30

@@ -8,9 +8,11 @@ unit) against the oracle.
     same bf16 operand (variant 1, only fp32 accumulation differs: <= 1e-5) and
     on the unrounded dequantisation (variant 0: <= 2e-2), for every code and
     block size;
-  - ragged K, M and even adapter ranks 2..40 (several 16-row passes), accumulation,
-    K = 0, and the Qwen2-7B-width MLP and hidden units (16384 x 18944 and
-    16384 x 3584, fp8 1x128, rank 16) on sampled columns.
+  - ragged K, M and even adapter ranks 2..98 (one-block passes and cooperative
+    passes of up to 80 rows, dh read in 16-byte chunks or in pairs),
+    accumulation, K = 0, and the Qwen2-7B-width MLP and hidden units (16384 x
+    18944 and 16384 x 3584, fp8 1x128, rank 16, and rank 80 on the hidden
+    unit) on sampled columns.
 """
 import numpy as np
 import pytest
@@ -37,9 +39,12 @@ def gpu_lora(hl, codes, scales, code, block, dh, scale=2.0, accumulate=False, da
     return host(da)
 
 
-def test_integer_exact(hl, orc):
-    g = np.random.default_rng(7)
-    K, M, r = 16384, 512, 16
+@pytest.mark.parametrize("r", [16, 42, 48, 80, 96])
+def test_integer_exact(hl, orc, r):
+    """Ranks above 16 run the cooperative kernel (passes of up to 80 rows: 96 is
+    80 + 16); 42 is not a multiple of 8, so its dh block is read in pairs."""
+    g = np.random.default_rng(7 + r)
+    K, M = 16384, 512
     q = g.integers(-7, 8, size=(K, M)) * 16
     codes = q.astype(np.int8).view(np.uint8)
     scales = np.full((K, M // 128), 1 / 16, dtype=np.float32)
@@ -74,7 +79,8 @@ def test_literal_cast(hl, orc):
 
 
 @pytest.mark.parametrize("K,M,r", [(1, 16, 16), (31, 272, 2), (33, 256, 8), (64, 4112, 18),
-                                   (517, 1040, 40), (2048, 256, 16), (95, 48, 32), (47, 528, 6)])
+                                   (517, 1040, 40), (2048, 256, 16), (95, 48, 32), (47, 528, 6),
+                                   (300, 528, 66), (1000, 256, 80), (65, 784, 98)])
 def test_ragged_shapes(hl, orc, K, M, r):
     """Widths that are multiples of 32 use E4M3FN with 32-wide blocks; the others
     (multiples of 16 only) use the literal cast, which has no blocks."""
@@ -87,8 +93,9 @@ def test_ragged_shapes(hl, orc, K, M, r):
     assert rel_fro(got, v1) <= 1e-5
 
 
-def test_accumulate_and_empty(hl, orc):
-    K, M, r = 300, 512, 16
+@pytest.mark.parametrize("r", [16, 48])
+def test_accumulate_and_empty(hl, orc, r):
+    K, M = 300, 512
     x = wl.activation_host(K, M, seed=120)
     codes, scales = orc.quantize(x, orc.INT8, 64)
     dh = wl.normal_bf16_host(K, r, seed=121, sigma=0.05)
@@ -127,15 +134,17 @@ def test_deterministic(hl, orc):
     assert_bytes_equal(a, b, "repeat")
 
 
-@pytest.mark.parametrize("M,unit", [(18944, 1), (3584, 0)], ids=["mlp_18944", "hidden_3584"])
-def test_qwen2_7b_units(hl, orc, M, unit):
+@pytest.mark.parametrize("M,unit,r", [(18944, 1, 16), (3584, 0, 16), (3584, 0, 80)],
+                         ids=["mlp_18944", "hidden_3584", "hidden_3584_qkvgu"])
+def test_qwen2_7b_units(hl, orc, M, unit, r):
     """The Qwen2-7B-width units at full size (16384 x 18944 MLP: 74 strips, the
     stream-K plan; 16384 x 3584 hidden: 14 strips, one workgroup per strip
-    part), fp8 1x128, rank-16 adapter: the first 2048 columns (8 strips) and
-    24 columns drawn from the rest, against the oracle on codes the oracle
-    recomputes."""
+    part), fp8 1x128, one rank-16 adapter, and on the hidden unit the five
+    rank-16 adapters that share it (q, k, v, gate, up: r = 80, one pass): the
+    first 2048 columns (8 strips) and 24 columns drawn from the rest, against
+    the oracle on codes the oracle recomputes."""
     w = wl.QWEN2_7B_LAYER
-    K, r, block, code = 16384, 16, 128, hl.HILORE_CODE_FP8_E4M3FN
+    K, block, code = 16384, 128, hl.HILORE_CODE_FP8_E4M3FN
     x = wl.activation_device(K, M, w.seed * 10 + unit, outliers=w.outliers)
     codes = torch.empty((K, M), dtype=torch.uint8, device="cuda")
     scales = torch.empty((K, M // block), dtype=torch.float32, device="cuda")
