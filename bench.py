@@ -626,18 +626,20 @@ def alloc_bench(hl, wl, iters=10):
     per, _ = timed_steps(step, 1, iters, 2)
     ms = med(per[0])
     a = action.cpu().numpy()
-    cells = (n_b + 1) * ((n_b + 1 + 63) // 64 * 64)
-    per_unit = cells * 16 + cells // 4  # read the previous table, write the next, 2-bit records
-    achieved = per_unit * inst.U / (ms * 1e-3) / 1e9
+    cells = (n_d + 1) * ((n_b + 1 + 63) // 64 * 64)
+    # one DP launch per pair of units: read the table before the pair, write the
+    # one after it, 2-bit records of both units
+    per_pair = cells * 16 + 2 * (cells // 4)
+    achieved = per_pair * (inst.U / 2) / (ms * 1e-3) / 1e9
     return {"units": inst.U, "grid": [n_b + 1, n_d + 1], "ms": round(ms, 4),
             "us_per_unit": round(ms * 1e3 / inst.U, 3),
-            "table_bytes_per_unit": per_unit,
+            "table_bytes_per_pair": per_pair,
             "roofline": {"kernel": "allocate_dp", "bound": "hbm", "achieved": round(achieved, 2),
                          "peak": HBM_PEAK_GBS, "unit": "GB/s",
                          "frac": round(achieved / HBM_PEAK_GBS, 4),
                          "traffic": TRAFFIC.get("alloc_196/allocate_dp"),
-                         "algorithmic": f"{per_unit} B per unit (one DP step); achieved over "
-                                        "the whole call, launches and backtrack included"},
+                         "algorithmic": f"{per_pair} B per DP launch (a pair of units); achieved "
+                                        "over the whole call, launches and backtrack included"},
             "chosen": {"R": int((a == 0).sum()), "H": int((a == 1).sum()),
                        "L": int((a == 2).sum())}}
 
@@ -688,6 +690,26 @@ def next_rows_bench(args, hl, wl, sets, code, block, rows, R):
                             what=f"{lb} B per call: codes + scales of {K}x{M}, dh {K}x{r} bf16, "
                                  f"dA {r}x{M} fp32")
     out["lora_grad"]["shape"] = {"K": K, "M": M, "r": r, "code": "fp8-e4m3fn", "block": block}
+    # the five rank-16 adapters that share one input (q, k, v or gate, up) in one call
+    r5 = 5 * r
+    dh5 = [wl.normal_bf16_device(K, r5, 520 + i, 0.05) for i in range(len(sets))]
+    da5 = torch.empty((r5, M), dtype=torch.float32, device="cuda")
+    ws5 = torch.empty(hl.hilore_lora_grad_workspace_bytes(K, M, r5), dtype=torch.uint8,
+                      device="cuda")
+
+    def lora5(i):
+        _, codes, scales, _, _, _ = sets[i]["keep"][1]
+        hl.hilore_dequant_lora_grad(codes, scales, code, block, dh5[i], da5, K, M, r5,
+                                    D.LORA_SCALE, False, ws5)
+
+    ms5 = timed(lora5)
+    lb5 = K * M + K * M * 4 // block + K * r5 * 2 + r5 * M * 4
+    out["lora_grad_5_adapters"] = {
+        "us": round(ms5 * 1e3, 2), "shape": {"K": K, "M": M, "r": r5},
+        "achieved_gbs": round(lb5 / (ms5 * 1e-3) / 1e9, 1),
+        "vs_one_adapter": round(ms5 / ms, 3),
+        "what": f"{r5} adapter rows (five rank-{r} adapters on one input) in one pass over the codes"}
+    del dh5, da5, ws5
     n = sets[0]["dw"].numel()
     y = torch.empty(1, dtype=torch.float32, device="cuda")
     wsr = torch.empty(hl.hilore_grad_rel_err_workspace_bytes(n), dtype=torch.uint8, device="cuda")

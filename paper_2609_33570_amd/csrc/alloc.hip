@@ -11,13 +11,14 @@
 //   F_i(j, k) = max over available a of F_{i-1}(j - b_i(a), k - r_i(a)) + tau_i(a)
 // runs over the (N_B + 1) x (N_delta + 1) grid of exact integer costs.
 //
-// Mapping.  One launch per unit updates the whole grid, one thread per cell
-// (rows k of risk cost, columns j of memory cost, a row padded to a multiple
-// of 64 cells so that a wave covers 64 consecutive cells of one row; each XCD
-// takes one contiguous band of cells).  Each
-// cell reads its own value and the two shifted sources from the previous
-// table (fp64, all in the 256 MB infinity cache for grids up to a few
-// thousand squared) and writes its new value; the chosen action (2 bits) is
+// Mapping.  One launch per pair of units updates the whole grid, one thread
+// per cell (rows k of risk cost, columns j of memory cost, a row padded to a
+// multiple of 64 cells so that a wave covers 64 consecutive cells of one row;
+// each XCD takes one contiguous band of cells).  Each cell forms the first
+// unit's value at itself and at the two cells the second unit's actions
+// shift it to, from up to nine cells of the table before the pair (fp64, all
+// in the 256 MB infinity cache for grids up to a few thousand squared), and
+// writes the value after the pair; the chosen action (2 bits) of each unit is
 // gathered across the wave with two ballots and stored as two 64-bit masks
 // per 64 cells, so the backtracking record of a 1025 x 1025 grid is 279 KB
 // per unit.  A reduction kernel then finds the best terminal cell, one wave
@@ -41,6 +42,10 @@ constexpr int kActR = 0, kActH = 1, kActL = 2;
 constexpr int kDpThreads = 256;
 constexpr int kPartials = 1024;  // workgroups of the terminal reduction
 constexpr int kFinalThreads = 1024;
+#ifndef HILORE_DP_GROUP
+#define HILORE_DP_GROUP 2
+#endif
+constexpr int kDpGroup = HILORE_DP_GROUP;  // units per DP launch (1 .. 4)
 
 // Availability of a non-R action (App. B.3 Eq. available-recovery-actions;
 // non-R actions with non-positive utility are excluded, App. B.2): verified,
@@ -96,49 +101,109 @@ __global__ void init_kernel(double *f, int64_t cells) {
   if (i < cells) f[i] = i == 0 ? 0.0 : -INFINITY;
 }
 
-// One unit of Eq. allocation-dp.  Actions are tried in the order R, H, L and
-// replace the incumbent only when strictly larger (the within-state tie
-// rule).  Padding cells (j >= KB) stay -inf.
-__global__ __launch_bounds__(kDpThreads) void dp_kernel(const double *__restrict__ prev,
-                                                         double *__restrict__ cur,
-                                                         uint64_t *__restrict__ pred,
-                                                         const AllocUnitCost *__restrict__ uc,
-                                                         int KB, int KD, int S) {
-  // Workgroups are dealt round-robin to the 8 XCDs; renumber them so that
-  // each XCD updates one contiguous band of the grid in every launch, and
-  // the previous table's band (and most shifted sources) is still in its L2.
-  const int n = (int)gridDim.x, x = (int)blockIdx.x & 7, q = n >> 3, rem = n & 7;
-  const int bid = x * q + (x < rem ? x : rem) + ((int)blockIdx.x >> 3);
-  const int64_t cell = (int64_t)bid * kDpThreads + threadIdx.x;
-  const int k = (int)(cell / S), j = (int)(cell % S);
-  if (k >= KD) return;  // whole waves: S and the grid are multiples of 64
-  const AllocUnitCost c = *uc;
-  double best = -INFINITY;
-  int act = kActR;
-  if (j < KB) {
-    best = prev[cell];
-    if (c.ok_h && c.b_h <= j) {
-      const double v = prev[cell - c.b_h] + c.tau_h;
+// F_i(j, k) of one unit of Eq. allocation-dp from the previous table: the
+// actions R, H, L in this order, each replacing the incumbent only when
+// strictly larger (the within-state tie rule); `act` receives the chosen
+// action.  The caller guarantees 0 <= j < KB and 0 <= k; padding cells
+// (j >= KB) stay -inf.
+__device__ __forceinline__ double unit_value(const double *__restrict__ prev,
+                                             const AllocUnitCost &c, int64_t cell, int j, int k,
+                                             int S, int &act) {
+  double best = prev[cell];
+  act = kActR;
+  if (c.ok_h && c.b_h <= j) {
+    const double v = prev[cell - c.b_h] + c.tau_h;
+    if (v > best) {
+      best = v;
+      act = kActH;
+    }
+  }
+  if (c.ok_l && c.b_l <= j && c.r_l <= k) {
+    const double v = prev[cell - (int64_t)c.r_l * S - c.b_l] + c.tau_l;
+    if (v > best) {
+      best = v;
+      act = kActL;
+    }
+  }
+  return best;
+}
+
+// F after the units c[0 .. N-1] (applied in order to the table `prev`) at
+// cell (j, k), by the rule of Eq. allocation-dp for the last unit applied to
+// the values after the first N - 1 at the cells its actions shift (j, k) to,
+// down to unit_value on `prev`.  Every value is formed by the same fp64
+// additions and comparisons, in the same order, as N single-unit launches
+// would form it.  With `acts`, acts[m] receives unit m's action at (j, k)
+// itself (the chain through the unshifted cell), i.e. its record there.
+template <int N>
+__device__ __forceinline__ double chain_value(const double *__restrict__ prev,
+                                              const AllocUnitCost *c, int64_t cell, int j, int k,
+                                              int S, int *acts) {
+  if constexpr (N == 1) {
+    int a;
+    const double v = unit_value(prev, c[0], cell, j, k, S, a);
+    if (acts) acts[0] = a;
+    return v;
+  } else {
+    double best = chain_value<N - 1>(prev, c, cell, j, k, S, acts);
+    int act = kActR;
+    const AllocUnitCost &u = c[N - 1];
+    if (u.ok_h && u.b_h <= j) {
+      const double v =
+          chain_value<N - 1>(prev, c, cell - u.b_h, j - u.b_h, k, S, nullptr) + u.tau_h;
       if (v > best) {
         best = v;
         act = kActH;
       }
     }
-    if (c.ok_l && c.b_l <= j && c.r_l <= k) {
-      const double v = prev[cell - (int64_t)c.r_l * S - c.b_l] + c.tau_l;
+    if (u.ok_l && u.b_l <= j && u.r_l <= k) {
+      const double v = chain_value<N - 1>(prev, c, cell - (int64_t)u.r_l * S - u.b_l,
+                                          j - u.b_l, k - u.r_l, S, nullptr) +
+                       u.tau_l;
       if (v > best) {
         best = v;
         act = kActL;
       }
     }
+    if (acts) acts[N - 1] = act;
+    return best;
   }
+}
+
+// N consecutive units of Eq. allocation-dp in one launch: each cell reads up
+// to 3^N cells of the table before the group (the shifted ones mostly from
+// the cache) and writes the table after it and the records of all N units,
+// bit for bit what N launches of one unit each would write; the tables in
+// between are never stored.
+template <int N>
+__global__ __launch_bounds__(kDpThreads) void dpn_kernel(const double *__restrict__ prev,
+                                                          double *__restrict__ cur,
+                                                          uint64_t *__restrict__ pred,
+                                                          size_t pred_words_per_unit,
+                                                          const AllocUnitCost *__restrict__ uc,
+                                                          int KB, int KD, int S) {
+  const int n = (int)gridDim.x, x = (int)blockIdx.x & 7, q = n >> 3, rem = n & 7;
+  const int bid = x * q + (x < rem ? x : rem) + ((int)blockIdx.x >> 3);
+  const int64_t cell = (int64_t)bid * kDpThreads + threadIdx.x;
+  const int k = (int)(cell / S), j = (int)(cell % S);
+  if (k >= KD) return;  // whole waves: S and the grid are multiples of 64
+  AllocUnitCost c[N];
+#pragma unroll
+  for (int m = 0; m < N; ++m) c[m] = uc[m];
+  int acts[N];
+#pragma unroll
+  for (int m = 0; m < N; ++m) acts[m] = kActR;
+  double best = -INFINITY;
+  if (j < KB) best = chain_value<N>(prev, c, cell, j, k, S, acts);
   cur[cell] = best;
-  const uint64_t lo = __ballot(act & 1);
-  const uint64_t hi = __ballot(act >> 1);
-  if ((threadIdx.x & (kWave - 1)) == 0) {
-    const int64_t w = cell / kWave;  // 64-cell chunk of this wave
-    pred[2 * w] = lo;
-    pred[2 * w + 1] = hi;
+  const int64_t w = cell / kWave;  // 64-cell chunk of this wave
+#pragma unroll
+  for (int m = 0; m < N; ++m) {
+    const uint64_t lo = __ballot(acts[m] & 1), hi = __ballot(acts[m] >> 1);
+    if ((threadIdx.x & (kWave - 1)) == 0) {
+      pred[m * pred_words_per_unit + 2 * w] = lo;
+      pred[m * pred_words_per_unit + 2 * w + 1] = hi;
+    }
   }
 }
 
@@ -366,15 +431,29 @@ hipError_t launch_allocate(const AllocArgs &a, int KB, int KD, void *workspace, 
   }
   const int grid = (int)((l.cells + kDpThreads - 1) / kDpThreads);
   hipLaunchKernelGGL(init_kernel, dim3(grid), dim3(kDpThreads), 0, s, f[0], l.cells);
-  for (int i = 0; i < a.U; ++i) {
-    hipLaunchKernelGGL(dp_kernel, dim3(grid), dim3(kDpThreads), 0, s, f[i & 1], f[(i + 1) & 1],
-                       reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(pred) +
-                                                    l.pred_bytes_per_unit * (size_t)i),
-                       uc + i, KB, KD, l.S);
+  auto pred_of = [&](int i) {
+    return reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(pred) +
+                                        l.pred_bytes_per_unit * (size_t)i);
+  };
+  // units in groups of kDpGroup (one launch each), the rest in a smaller
+  // group; the table after launch t lives in f[t & 1]
+  const size_t words = l.pred_bytes_per_unit / sizeof(uint64_t);
+  int t = 0;
+  for (int i = 0; i < a.U; i += kDpGroup, ++t) {
+    const int g = a.U - i < kDpGroup ? a.U - i : kDpGroup;
+    const dim3 gd(grid), bd(kDpThreads);
+    double *src = f[t & 1], *dst = f[(t + 1) & 1];
+    uint64_t *pr = pred_of(i);
+    switch (g) {
+      case 1: hipLaunchKernelGGL(dpn_kernel<1>, gd, bd, 0, s, src, dst, pr, words, uc + i, KB, KD, l.S); break;
+      case 2: hipLaunchKernelGGL(dpn_kernel<2>, gd, bd, 0, s, src, dst, pr, words, uc + i, KB, KD, l.S); break;
+      case 3: hipLaunchKernelGGL(dpn_kernel<3>, gd, bd, 0, s, src, dst, pr, words, uc + i, KB, KD, l.S); break;
+      default: hipLaunchKernelGGL(dpn_kernel<4>, gd, bd, 0, s, src, dst, pr, words, uc + i, KB, KD, l.S); break;
+    }
   }
   const int n_partial = grid < kPartials ? grid : kPartials;
   hipLaunchKernelGGL(terminal_partial_kernel, dim3(n_partial), dim3(kDpThreads), 0, s,
-                     f[a.U & 1], l.cells, partial);
+                     f[t & 1], l.cells, partial);
   hipLaunchKernelGGL(terminal_backtrack_kernel, dim3(1), dim3(kFinalThreads), 0, s, a, partial,
                      n_partial, pred, uc, l.S, KD);
   hipLaunchKernelGGL(totals_kernel, dim3(1), dim3(kWave), 0, s, a);
