@@ -89,16 +89,51 @@ __global__ void costs_kernel(const AllocArgs a, AllocUnitCost *uc) {
   c.b_h = (int32_t)b_h;
   c.b_l = (int32_t)b_l;
   c.r_l = (int32_t)r_l;
-  c.pad = 0;
+  c.reach = 0;  // set by reach_kernel
   c.tau_h = a.tau_h[u];
   c.tau_l = a.tau_l[u];
   uc[u] = c;
 }
 
-// F_0: 0 at (0, 0), -inf elsewhere (padding cells included).
-__global__ void init_kernel(double *f, int64_t cells) {
+// Memory cost reach after each unit: the running sum, in unit order, of the
+// largest memory cost of each unit's available actions, capped at KB - 1
+// (integers, one workgroup: a scan per chunk of 1024 units plus a carry).
+// No state after unit i has a memory cost above uc[i].reach.
+constexpr int kReachThreads = 1024;
+__global__ __launch_bounds__(kReachThreads) void reach_kernel(AllocUnitCost *uc, int U, int KB) {
+  __shared__ int part[kReachThreads];
+  const int tid = (int)threadIdx.x;
+  int carry = 0;
+  for (int base = 0; base < U; base += kReachThreads) {
+    const int i = base + tid;
+    int v = 0;
+    if (i < U) {
+      const AllocUnitCost c = uc[i];
+      v = max(c.ok_h ? c.b_h : 0, c.ok_l ? c.b_l : 0);  // each at most KB
+    }
+    part[tid] = v;
+    __syncthreads();
+    for (int off = 1; off < kReachThreads; off <<= 1) {
+      const int t = tid >= off ? part[tid - off] : 0;
+      __syncthreads();
+      part[tid] += t;  // at most 1024 * KB: no overflow for KB <= 4097
+      __syncthreads();
+    }
+    if (i < U) uc[i].reach = min(KB - 1, carry + part[tid]);
+    carry = min(KB, carry + part[kReachThreads - 1]);
+    __syncthreads();
+  }
+}
+
+// F_0: 0 at (0, 0), -inf elsewhere (padding cells included), and the second
+// table all -inf: a DP launch skips the waves whose cells lie beyond the
+// memory cost reach, which must then read as unreachable in either table.
+__global__ void init_kernel(double *f0, double *f1, int64_t cells) {
   const int64_t i = (int64_t)blockIdx.x * blockDim.x + threadIdx.x;
-  if (i < cells) f[i] = i == 0 ? 0.0 : -INFINITY;
+  if (i < cells) {
+    f0[i] = i == 0 ? 0.0 : -INFINITY;
+    f1[i] = -INFINITY;
+  }
 }
 
 // F_i(j, k) of one unit of Eq. allocation-dp from the previous table: the
@@ -190,6 +225,11 @@ __global__ __launch_bounds__(kDpThreads) void dpn_kernel(const double *__restric
   AllocUnitCost c[N];
 #pragma unroll
   for (int m = 0; m < N; ++m) c[m] = uc[m];
+  // A wave (64 consecutive cells of one row) wholly beyond the memory cost
+  // reach after the group holds only unreachable states: they stay -inf in
+  // both tables, and no path the backtrack follows passes through them, so
+  // neither their values nor their records are written.
+  if (__builtin_amdgcn_readfirstlane(j) > c[N - 1].reach) return;
   int acts[N];
 #pragma unroll
   for (int m = 0; m < N; ++m) acts[m] = kActR;
@@ -428,9 +468,10 @@ hipError_t launch_allocate(const AllocArgs &a, int KB, int KD, void *workspace, 
 
   if (a.U > 0) {
     hipLaunchKernelGGL(costs_kernel, dim3((a.U + 255) / 256), dim3(256), 0, s, a, uc);
+    hipLaunchKernelGGL(reach_kernel, dim3(1), dim3(kReachThreads), 0, s, uc, a.U, KB);
   }
   const int grid = (int)((l.cells + kDpThreads - 1) / kDpThreads);
-  hipLaunchKernelGGL(init_kernel, dim3(grid), dim3(kDpThreads), 0, s, f[0], l.cells);
+  hipLaunchKernelGGL(init_kernel, dim3(grid), dim3(kDpThreads), 0, s, f[0], f[1], l.cells);
   auto pred_of = [&](int i) {
     return reinterpret_cast<uint64_t *>(reinterpret_cast<char *>(pred) +
                                         l.pred_bytes_per_unit * (size_t)i);

@@ -132,7 +132,8 @@ struct AllocArgs {
 };
 struct AllocUnitCost {  // integer costs of one unit on the grid
   int32_t ok_h, ok_l;
-  int32_t b_h, b_l, r_l, pad;
+  int32_t b_h, b_l, r_l;
+  int32_t reach;  // largest memory cost of any state after this unit (cumulative, < KB)
   double tau_h, tau_l;
 };
 struct AllocLayout {  // the caller's workspace, carved into 256-byte aligned parts
