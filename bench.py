@@ -103,6 +103,7 @@ def risk_bytes(rows, units, masked):
 KERNEL_SOURCES = {"compress": ["codec.hip"], "decompress": ["codec.hip"],
                   "dequant_wgrad": ["wgrad.hip"], "grpo_coeffs": ["grpo.hip"],
                   "exposure_risk": ["risk.hip"], "dequant_lora_grad": ["lora.hip"],
+                  "dequant_lora_grad_5": ["lora.hip"],
                   "grad_rel_err": ["calib.hip"], "dequant_swiglu_bwd": ["swiglu.hip"],
                   "allocate_dp": ["alloc.hip"]}
 
