@@ -369,10 +369,10 @@ struct CoopLd {
   u32x4 d;
 };
 
-template <int CODE, int BLOCK, int R, bool WIDE>
+template <int CODE, int BLOCK, bool WIDE>
 __device__ __forceinline__ void coop_load(CoopLd &l, const LoraArgs &a, uint32_t vo_c,
                                           uint32_t vo_s, const uint32_t (&vo_d)[3], int64_t kk,
-                                          bool live, int tid) {
+                                          bool live) {
   const int64_t rows = step_rows(a, kk, live);
   const int64_t t0 = kk * kStep;
   const __amdgpu_buffer_rsrc_t rc = __builtin_amdgcn_make_buffer_rsrc(
@@ -385,14 +385,17 @@ __device__ __forceinline__ void coop_load(CoopLd &l, const LoraArgs &a, uint32_t
         (void *)(a.scales + t0 * sld), 0, (int)(rows * sld * 4), 0x00020000);
     l.s = __uint_as_float(__builtin_amdgcn_raw_buffer_load_b32(rs, (int)vo_s, 0, 0));
   }
+  // Every thread issues the same loads (threads past the dh block have the
+  // out-of-range offset and read 0): a load behind a per-thread condition
+  // becomes a branch, and the compiler then drains every load in flight at
+  // the loop head instead of keeping D k-steps outstanding.
   const __amdgpu_buffer_rsrc_t rd = dh_rsrc(a, t0, rows);
   if constexpr (WIDE) {
-    if (tid < 64 * R)
-      l.d = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rd, (int)vo_d[0], 0, 0));
+    l.d = __builtin_bit_cast(u32x4, __builtin_amdgcn_raw_buffer_load_b128(rd, (int)vo_d[0], 0, 0));
   } else {
     l.d.x = __builtin_amdgcn_raw_buffer_load_b32(rd, (int)vo_d[0], 0, 0);
-    if (tid + 512 < 256 * R) l.d.y = __builtin_amdgcn_raw_buffer_load_b32(rd, (int)vo_d[1], 0, 0);
-    if (tid + 1024 < 256 * R) l.d.z = __builtin_amdgcn_raw_buffer_load_b32(rd, (int)vo_d[2], 0, 0);
+    l.d.y = __builtin_amdgcn_raw_buffer_load_b32(rd, (int)vo_d[1], 0, 0);
+    l.d.z = __builtin_amdgcn_raw_buffer_load_b32(rd, (int)vo_d[2], 0, 0);
   }
 }
 
@@ -472,7 +475,7 @@ __global__ __launch_bounds__(kThreads, 1) void lora_coop_kernel(const LoraArgs a
     CoopLd L[D];
 #pragma unroll
     for (int i = 0; i < D; ++i)
-      coop_load<CODE, BLOCK, R, WIDE>(L[i], a, vo_c, vo_s, vo_d, k0 + i, k0 + i < k_end, tid);
+      coop_load<CODE, BLOCK, WIDE>(L[i], a, vo_c, vo_s, vo_d, k0 + i, k0 + i < k_end);
 
     for (int64_t kb = k0; kb < k_end; kb += D) {
 #pragma unroll
@@ -506,9 +509,8 @@ __global__ __launch_bounds__(kThreads, 1) void lora_coop_kernel(const LoraArgs a
             if (tid + 1024 < 256 * R) *reinterpret_cast<uint32_t *>(db + 4 * (tid + 1024)) = l.d.z;
           }
         }
-        coop_load<CODE, BLOCK, R, WIDE>(L[i], a, vo_c, vo_s, vo_d, k + D, k + D < k_end, tid);
-        coop_load<CODE, BLOCK, R, WIDE>(L[i + 1], a, vo_c, vo_s, vo_d, k + 1 + D, k + 1 + D < k_end,
-                                        tid);
+        coop_load<CODE, BLOCK, WIDE>(L[i], a, vo_c, vo_s, vo_d, k + D, k + D < k_end);
+        coop_load<CODE, BLOCK, WIDE>(L[i + 1], a, vo_c, vo_s, vo_d, k + 1 + D, k + 1 + D < k_end);
         // both tiles written; the reads of this buffer two rounds ago are done
         __syncthreads();
 #pragma unroll
