@@ -329,17 +329,34 @@ __global__ __launch_bounds__(kFinalThreads) void terminal_backtrack_kernel(
     a.totals[0] = b.v;
   }
   const int64_t chunks = S / kWave;
-  // this lane's depth d and path p
+  // this lane's depth d and path p, and the base-3 digits of p (unit i's
+  // action first)
   const int d = lane == 0 ? 0 : lane < 4 ? 1 : lane < 13 ? 2 : 3;
   const int p = lane - (d == 0 ? 0 : d == 1 ? 1 : d == 2 ? 4 : 13);
-  auto load_costs = [&](int unit, int &bh, int &bl, int &rl) {
-    bh = bl = rl = 0;
-    if (lane < kLookUnits && unit - lane >= 0) {
-      const AllocUnitCost c = uc[unit - lane];
-      bh = c.b_h;
-      bl = c.b_l;
-      rl = c.r_l;
+  int digit[3];
+  {
+    int rest = p, pw = d == 3 ? 9 : d == 2 ? 3 : 1;
+#pragma unroll
+    for (int m = 0; m < 3; ++m) {
+      digit[m] = m < d ? rest / pw : kActR;
+      if (m < d) {
+        rest -= digit[m] * pw;
+        pw /= 3;
+      }
     }
+  }
+  // Every load below is issued unconditionally (a lane with nothing to load
+  // reads a valid dummy address and discards the value), so that no branch
+  // forces a wait: the costs of the next four units are waited for only in
+  // the next round trip, and the record load is the one latency per trip.
+  const bool cost_lane = lane < kLookUnits;
+  auto load_costs = [&](int unit, int &bh, int &bl, int &rl) {
+    const bool ok = cost_lane && unit - lane >= 0;
+    const AllocUnitCost &c = uc[ok ? unit - lane : 0];
+    const int h = c.b_h, l = c.b_l, r = c.r_l;
+    bh = ok ? h : 0;
+    bl = ok ? l : 0;
+    rl = ok ? r : 0;
   };
   int bh, bl, rl;
   load_costs(a.U - 1, bh, bl, rl);
@@ -349,25 +366,18 @@ __global__ __launch_bounds__(kFinalThreads) void terminal_backtrack_kernel(
     // the cell of this lane's record: the current cell minus the costs of
     // the actions its path takes at units i .. i - d + 1
     int64_t jj = j, kk = k;
-    int rest = p;
-    int pw = d == 3 ? 9 : d == 2 ? 3 : 1;
 #pragma unroll
     for (int m = 0; m < 3; ++m) {
       const int ubh = lane_int(bh, m), ubl = lane_int(bl, m), url = lane_int(rl, m);
-      if (m < d) {
-        const int digit = rest / pw;
-        rest -= digit * pw;
-        pw /= 3;
-        if (digit == kActH) jj -= ubh;
-        if (digit == kActL) {
-          jj -= ubl;
-          kk -= url;
-        }
+      if (digit[m] == kActH) jj -= ubh;
+      if (digit[m] == kActL) {
+        jj -= ubl;
+        kk -= url;
       }
     }
-    int act = kActR;
-    if (lane < kLookLanes && i - d >= 0 && jj >= 0 && kk >= 0)
-      act = record(pred, i - d, kk, jj, KD, chunks);
+    const bool rec = lane < kLookLanes && i - d >= 0 && jj >= 0 && kk >= 0;
+    const int r = record(pred, rec ? i - d : 0, rec ? kk : 0, rec ? jj : 0, KD, chunks);
+    const int act = rec ? r : kActR;
     const int a0 = lane_int(act, 0);
     const int a1 = lane_int(act, 1 + a0);
     const int a2 = lane_int(act, 4 + 3 * a0 + a1);
