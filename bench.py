@@ -927,6 +927,44 @@ def cpu_baseline(hl, wl, smp, plan_sample, stress_sample, runs=3):
     }
 
 
+def copy_peak():
+    """A plain device-to-device copy of 1 GiB (torch's copy_, 1 GiB read and 1 GiB
+    written, median of 10): the streaming rate this GPU reaches in practice, which
+    each HBM-bound roofline is also read against ("frac_copy")."""
+    import torch
+    n = 1 << 29  # bf16 elements: 1 GiB
+    src = torch.ones(n, dtype=torch.bfloat16, device="cuda")
+    dst = torch.empty_like(src)
+    for _ in range(3):
+        dst.copy_(src)
+    torch.cuda.synchronize()
+    ts = []
+    for _ in range(10):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        dst.copy_(src)
+        e1.record()
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    del src, dst
+    torch.cuda.empty_cache()
+    gbs = 2 * 2 * n / (med(ts) * 1e-3) / 1e9
+    return {"gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
+            "what": "torch copy_ of 1 GiB bf16 (1 GiB read + 1 GiB written), median of 10"}
+
+
+def add_copy_fractions(o, copy_gbs):
+    """Add achieved / copy peak next to every HBM-bound roofline in the line."""
+    if isinstance(o, dict):
+        if o.get("bound") == "hbm" and isinstance(o.get("achieved"), (int, float)):
+            o["frac_copy"] = round(o["achieved"] / copy_gbs, 4)
+        for v in o.values():
+            add_copy_fractions(v, copy_gbs)
+    elif isinstance(o, list):
+        for v in o:
+            add_copy_fractions(v, copy_gbs)
+
+
 def main():
     args = parse()
     if args.gpus != 1:
@@ -988,6 +1026,9 @@ def main():
                         f"llama3_8b_stress_T{T}") for T in (sw.T, 2 * sw.T)]
         out["configs"]["llama3_8b_stress"] = stress
         out["coeff_sweep"] = coeff_sweep(args, hl, wl)
+    progress("copy peak: 1 GiB device-to-device")
+    out["copy_peak"] = copy_peak()
+    add_copy_fractions(out, out["copy_peak"]["gbs"])
     if smp is not None:
         progress("timing the oracle on the host")
         if plan_sample is None:
