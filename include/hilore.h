@@ -364,7 +364,7 @@ hilore_status hilore_dequant_swiglu_bwd(const hilore_unit_desc *gate, const hilo
  *              hilore_calibrate)
  * The sums are fp64 over the fp32 values, in a fixed order (per-workgroup partial
  * sums in `workspace`, then one fixed tree).  workspace: device memory of at least
- * hilore_grad_rel_err_workspace_bytes(n) bytes (at most 256 KB), 16-byte aligned;
+ * hilore_grad_rel_err_workspace_bytes(n) bytes (at most 16 KB), 16-byte aligned;
  * its contents on entry do not matter; calls sharing it must not overlap.
  * n = 0 gives y = 0.  Errors: n < 0, eps_num not positive and finite, null
  * pointers -> INVALID_ARG; workspace too small -> WORKSPACE.

@@ -150,7 +150,7 @@ hipError_t launch_allocate(const AllocArgs &a, int KB, int KD, void *workspace, 
 
 // Calibration scalars (App. B.1 Eqs. app-calibration-error, app-kappa,
 // app-risk-score) and the update-sparsity diagnostics (App. D.3).
-constexpr int kRelMaxPartials = 16384;  // workgroups of the relative-error reduction
+constexpr int kRelMaxPartials = 1024;  // workgroups of the relative-error reduction (4 per CU)
 int rel_err_partials(int64_t n);       // how many of them a reduction over n uses
 hipError_t launch_grad_rel_err(const float *g_l, const float *g_ex, int64_t n, double eps_num,
                                float *y, double *part, hipStream_t s);

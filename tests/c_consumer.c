@@ -24,7 +24,7 @@ int main(void) {
 
   /* workspace queries */
   expect("grad_rel_err workspace, n = 2^24", (long)hilore_grad_rel_err_workspace_bytes(1 << 24),
-         4096 * 16);
+         1024 * 16);
   expect("allocate workspace, bad grid", (long)hilore_allocate_workspace_bytes(4, 0, 16), 0);
   expect("lora workspace, r = 0", (long)hilore_lora_grad_workspace_bytes(1024, 256, 0), 0);
 

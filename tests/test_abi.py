@@ -260,7 +260,7 @@ def test_calibration_entry_points_validate(lib):
     E = hilore
     big = 1 << 20
     ws = lib.hilore_grad_rel_err_workspace_bytes
-    assert ws(0) == 16 and ws(1 << 24) == 4096 * 16 and ws(1 << 30) == 16384 * 16 and ws(-1) == 0
+    assert ws(0) == 16 and ws(1 << 20) == 256 * 16 and ws(1 << 24) == 1024 * 16 and ws(1 << 30) == 1024 * 16 and ws(-1) == 0
     rel = lib.hilore_grad_rel_err
     assert rel(FAKE, FAKE, 1000, 1e-30, FAKE, FAKE, 15, None) == E.HILORE_ERR_WORKSPACE
     assert rel(FAKE, FAKE, -1, 1e-30, FAKE, FAKE, big, None) == E.HILORE_ERR_INVALID_ARG

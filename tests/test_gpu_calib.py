@@ -69,8 +69,9 @@ def test_grad_rel_err_dw_sized(hl, orc):
 
 
 def test_grad_rel_err_beyond_one_pass(hl, orc):
-    """More 16 KiB chunks than partial slots (4 * 16384 * 1024 floats plus a
-    ragged chunk and a 3-element tail): workgroups then take a second chunk."""
+    """Many more 16 KiB chunks than partial slots (4 * 16384 * 1024 floats plus
+    a ragged chunk and a 3-element tail: 65537 chunks over 1024 workgroups, so
+    each streams 64 or 65 of them)."""
     n = 4 * 16384 * 1024 + 4096 + 3
     g = torch.Generator(device="cuda")
     g.manual_seed(wl.BASE_SEED + 52)
@@ -78,7 +79,7 @@ def test_grad_rel_err_beyond_one_pass(hl, orc):
     lo = ex + torch.randn(n, generator=g, device="cuda") * 1e-2
     ws = torch.empty(hl.hilore_grad_rel_err_workspace_bytes(n) // 8, dtype=torch.float64,
                      device="cuda")
-    assert ws.numel() == 2 * 16384
+    assert ws.numel() == 2 * 1024
     y = filled(1, torch.float32, float("nan"))
     hl.hilore_grad_rel_err(lo, ex, y, ws)
     torch.cuda.synchronize()
