@@ -928,29 +928,37 @@ def cpu_baseline(hl, wl, smp, plan_sample, stress_sample, runs=3):
 
 
 def copy_peak():
-    """A plain device-to-device copy of 1 GiB (torch's copy_, 1 GiB read and 1 GiB
-    written, median of 10): the streaming rate this GPU reaches in practice, which
-    each HBM-bound roofline is also read against ("frac_copy")."""
+    """The streaming rate this GPU reaches with a plain copy of 1 GiB (1 GiB read
+    and 1 GiB written, median of 10), which each HBM-bound roofline is also read
+    against ("frac_copy"): torch's elementwise kernel (x * 1.0 in bf16, an exact
+    copy) and, for reference, the runtime's device-to-device blit (copy_)."""
     import torch
     n = 1 << 29  # bf16 elements: 1 GiB
     src = torch.ones(n, dtype=torch.bfloat16, device="cuda")
     dst = torch.empty_like(src)
-    for _ in range(3):
-        dst.copy_(src)
-    torch.cuda.synchronize()
-    ts = []
-    for _ in range(10):
-        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
-        e0.record()
-        dst.copy_(src)
-        e1.record()
-        e1.synchronize()
-        ts.append(e0.elapsed_time(e1))
+
+    def rate(fn):
+        for _ in range(3):
+            fn()
+        torch.cuda.synchronize()
+        ts = []
+        for _ in range(10):
+            e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+            e0.record()
+            fn()
+            e1.record()
+            e1.synchronize()
+            ts.append(e0.elapsed_time(e1))
+        return 2 * 2 * n / (med(ts) * 1e-3) / 1e9
+
+    elementwise = rate(lambda: torch.mul(src, 1.0, out=dst))
+    blit = rate(lambda: dst.copy_(src))
     del src, dst
     torch.cuda.empty_cache()
-    gbs = 2 * 2 * n / (med(ts) * 1e-3) / 1e9
-    return {"gbs": round(gbs, 1), "frac_of_peak": round(gbs / HBM_PEAK_GBS, 4),
-            "what": "torch copy_ of 1 GiB bf16 (1 GiB read + 1 GiB written), median of 10"}
+    return {"gbs": round(elementwise, 1), "frac_of_peak": round(elementwise / HBM_PEAK_GBS, 4),
+            "blit_gbs": round(blit, 1),
+            "what": "1 GiB bf16 copied by torch's elementwise kernel (x * 1.0), 1 GiB read + "
+                    "1 GiB written, median of 10; blit_gbs: the runtime's device-to-device copy_"}
 
 
 def add_copy_fractions(o, copy_gbs):
