@@ -119,3 +119,14 @@ def test_many_units(hl, orc, integer):
     inst = wl.alloc_small(1001, seed=4242 + integer, integer=integer, scale=8.0)
     assert_same(gpu_allocate(hl, inst, 64, 48), oracle_allocate(orc, inst, 64, 48),
                 f"U=1001 integer={integer}")
+
+
+@pytest.mark.parametrize("grid", [(4096, 4096), (4095, 4093)], ids=["max", "max-ragged"])
+def test_largest_grid(hl, orc, grid):
+    """The largest grid the entry point accepts (N_B = N_delta = 4096 intervals:
+    4097 x 4097 states, rows padded to 4160 cells) and a ragged one just below
+    it, with units costly enough that the reach crosses many 64-cell chunks."""
+    n_b, n_d = grid
+    inst = wl.alloc_small(12, seed=9000 + n_b + n_d, scale=8.0)
+    assert_same(gpu_allocate(hl, inst, n_b, n_d), oracle_allocate(orc, inst, n_b, n_d),
+                f"grid {grid}")
