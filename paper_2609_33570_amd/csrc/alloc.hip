@@ -437,8 +437,10 @@ __global__ __launch_bounds__(kWave) void totals_kernel(const AllocArgs a) {
   UnitTotals c = unit_costs(a, lane);
   for (int base = 0; base < a.U; base += kWave) {
     const UnitTotals next = unit_costs(a, base + kWave + lane);
-    const int n = a.U - base < kWave ? a.U - base : kWave;
-    for (int t = 0; t < n; ++t) {
+    // all 64 lanes, unrolled (constant lane indices): lanes past the last
+    // unit hold +0.0, which leaves the sums unchanged
+#pragma unroll
+    for (int t = 0; t < kWave; ++t) {
       mem += lane_f64(c.mem, t);
       risk += lane_f64(c.risk, t);
     }
