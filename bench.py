@@ -660,7 +660,7 @@ def next_rows_bench(args, hl, wl, sets, code, block, rows, R):
     import numpy as np
     import torch
 
-    key = "qwen2_7b_layer"
+    key = "qwen2_7b_layer_next"  # the profiles' name for these calls on the layer's data
 
     def timed(fn, iters=20):
         def step(i, mark):
@@ -709,6 +709,7 @@ def next_rows_bench(args, hl, wl, sets, code, block, rows, R):
         "us": round(ms5 * 1e3, 2), "shape": {"K": K, "M": M, "r": r5},
         "achieved_gbs": round(lb5 / (ms5 * 1e-3) / 1e9, 1),
         "vs_one_adapter": round(ms5 / ms, 3),
+        "traffic": TRAFFIC.get(f"{key}/dequant_lora_grad_5"),
         "what": f"{r5} adapter rows (five rank-{r} adapters on one input) in one pass over the codes"}
     del dh5, da5, ws5
     n = sets[0]["dw"].numel()
