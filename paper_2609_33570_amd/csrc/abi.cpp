@@ -85,9 +85,10 @@ hilore_status run_codec(const hilore_unit_desc *units, int n_units, int code, in
     if (st != HILORE_OK) return st;
   }
   // consecutive units that share a row mapping go to one launch (at most
-  // kUnitsPerLaunch units and kRowsPerLaunch rows per launch)
+  // kUnitsPerLaunch units, kRowsPerLaunch rows and, unless one unit alone is
+  // larger, kElemsPerLaunch elements per launch)
   CodecBatch b{};
-  int64_t rows = 0;
+  int64_t rows = 0, elems = 0;
   bool any_stats = false;
   auto flush = [&]() -> hilore_status {
     if (b.n == 0) return HILORE_OK;
@@ -98,6 +99,7 @@ hilore_status run_codec(const hilore_unit_desc *units, int n_units, int code, in
     b = CodecBatch{};
     b.wpr_log2 = wl;
     rows = 0;
+    elems = 0;
     any_stats = false;
     return st;
   };
@@ -106,7 +108,8 @@ hilore_status run_codec(const hilore_unit_desc *units, int n_units, int code, in
     if (u.rows == 0 || u.cols == 0) continue;
     const int wl = hilore::codec_wpr_log2(u.cols, lane_steps);
     if (b.n == hilore::kUnitsPerLaunch || (b.n > 0 && wl != b.wpr_log2) ||
-        rows + u.rows > hilore::kRowsPerLaunch) {
+        rows + u.rows > hilore::kRowsPerLaunch ||
+        (b.n > 0 && elems + u.rows * u.cols > hilore::kElemsPerLaunch)) {
       const hilore_status st = flush();
       if (st != HILORE_OK) return st;
     }
@@ -124,6 +127,7 @@ hilore_status run_codec(const hilore_unit_desc *units, int n_units, int code, in
     any_stats = any_stats || c.ss_x || c.ss_err;
     b.row_begin[b.n] = rows;
     rows += u.rows;
+    elems += u.rows * u.cols;
     ++b.n;
   }
   return flush();

@@ -156,6 +156,42 @@ def test_many_units_one_call(hl, orc):
         check_unit(orc, x, r, 1, 128, what=f"unit {i}")
 
 
+def test_launches_split_by_element_count(hl):
+    """Six 4096 x 16384 units (2^26 elements each) in one call: the library
+    puts at most 2^28 elements in a launch, so they go out as launches of 4
+    and 2 units; every output must equal that of six single-unit calls, byte
+    for byte (codes, scales, reconstruction and both row sums)."""
+    rows, cols, code, block = 4096, 16384, 1, 128
+    xs = [wl.activation_device(rows, cols, 6100 + i) for i in range(6)]
+
+    def outputs():
+        return dict(codes=filled((rows, cols), torch.uint8, 0xEE),
+                    scales=filled((rows, cols // block), torch.float32, float("nan")),
+                    xhat=filled((rows, cols), torch.int16, 0x7FC1),
+                    ssx=filled((rows,), torch.float32, float("nan")),
+                    sse=filled((rows,), torch.float32, float("nan")))
+
+    def descs(x, o):
+        return (hl.unit_desc(x=x, codes=o["codes"], scales=o["scales"], row_ss_x=o["ssx"],
+                             row_ss_err=o["sse"]),
+                hl.unit_desc(codes=o["codes"], scales=o["scales"], xhat=o["xhat"], rows=rows,
+                             cols=cols))
+
+    batched = [outputs() for _ in xs]
+    d = [descs(x, o) for x, o in zip(xs, batched)]
+    hl.hilore_compress([c for c, _ in d], code, block)
+    hl.hilore_decompress([r for _, r in d], code, block)
+    for x, o0 in zip(xs, batched):
+        o = outputs()
+        c, r = descs(x, o)
+        hl.hilore_compress([c], code, block)
+        hl.hilore_decompress([r], code, block)
+        torch.cuda.synchronize()
+        for k in o:
+            assert torch.equal(o0[k].view(torch.uint8), o[k].view(torch.uint8)), k
+        del o
+
+
 def test_without_stats(hl, orc):
     x = wl.activation_host(64, 1024, seed=8)
     (res,) = gpu_codec(hl, [x], 0, 128, stats=False)

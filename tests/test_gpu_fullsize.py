@@ -165,9 +165,11 @@ def test_qwen2_7b_plan(hl, orc):
     g = np.random.default_rng(2)
     for i, u in enumerate(units):
         check_rows(orc, u, np.sort(g.choice(rows, 6, replace=False)), code, block, f"unit {i}")
-    # the batched call encodes 16 units per launch: one whole unit of every launch
-    for i in range(0, n, 16):
-        check_unit(orc, units[i], code, block, f"unit {i} (launch {i // 16})")
+    # the batched call puts at most 2^28 elements (4 of these units) in a
+    # launch: one whole unit of every launch
+    per = min(16, max(1, (1 << 28) // (rows * 3584)))
+    for i in range(0, n, per):
+        check_unit(orc, units[i], code, block, f"unit {i} (launch {i // per})")
     ge, gk, gr = host(expo), host(risk), host(rel)
     for i in (0, n - 1):  # two units end to end against the oracle
         x = host(units[i]["x"])
@@ -225,8 +227,8 @@ def test_llama3_8b_stress(hl, orc):
     the 30%-padded GRPO batch (N counted in the launch), one batched compress
     with row sums of the 32 units, exposure/risk under the length mask, one
     batched decompress.  Checked: flags and advantages bit for bit and the
-    coefficients to tolerance; two whole units (one of each 16-unit launch)
-    row for row against the oracle, sampled rows of every other unit; every
+    coefficients to tolerance; two whole units (each of these units is a
+    launch of its own: it exceeds the 2^28-element batching bound) row for row against the oracle, sampled rows of every other unit; every
     unit's exposure/risk/rel_err from its GPU row sums in fp64, and for the
     two whole units from the oracle's own row sums."""
     w = wl.LLAMA3_8B_STRESS
