@@ -928,6 +928,36 @@ def cpu_baseline(hl, wl, smp, plan_sample, stress_sample, runs=3):
     }
 
 
+def wgrad_standalone(hl, sets, code, block, K, M, N, iters=20):
+    """The fused wgrad call of the step timed back to back over the rotating
+    buffer sets (median of per-call events), outside the step: the kernel's
+    own rate, without the decompress that precedes it in the step."""
+    import torch
+
+    def call(i):
+        st = sets[i % len(sets)]
+        hl.hilore_dequant_wgrad(st["wc"], st["ws"], code, block, st["dy"], st["dw"], K, M, N,
+                                False)
+
+    for i in range(3):
+        call(i)
+    torch.cuda.synchronize()
+    ts = []
+    for i in range(iters):
+        e0, e1 = torch.cuda.Event(enable_timing=True), torch.cuda.Event(enable_timing=True)
+        e0.record()
+        call(i)
+        e1.record()
+        e1.synchronize()
+        ts.append(e0.elapsed_time(e1))
+    ms = med(ts)
+    tf = 2.0 * K * M * N / (ms * 1e-3) / 1e12
+    return {"tflops": round(tf, 2), "frac_mfma": round(tf / BF16_PEAK_TFLOPS, 4),
+            "us": round(ms * 1e3, 2),
+            "what": f"the same call back to back over the {len(sets)} rotating buffer sets "
+                    f"({iters} calls, median), outside the step"}
+
+
 def copy_peak():
     """The streaming rate this GPU reaches with a plain copy of 1 GiB (1 GiB read
     and 1 GiB written, median of 10), which each HBM-bound roofline is also read
@@ -1004,6 +1034,10 @@ def main():
         out["allocate"] = alloc_bench(hl, wl)
         progress("context calls: LoRA adapter gradient, calibration and diagnostics")
         out["next"] = next_rows_bench(args, hl, wl, sets, code, block, R * w.T, R)
+    wg_alone = None
+    if not args.step_only:
+        progress("the fused wgrad back to back, outside the step")
+        wg_alone = wgrad_standalone(hl, sets, code, block, *ww.wgrad)
     if args.blas_ref:
         progress("timing hipBLASLt on the reconstructed X")
         out["blas_ref"] = blas_ref(sets[0], code, block, *ww.wgrad)
@@ -1024,7 +1058,7 @@ def main():
                                "see": "the headline step"},
             "wgrad_4096": {"workload": "wgrad_4096", "tflops": out["wgrad_tflops"],
                            "frac_mfma": out["wgrad_frac_mfma"], "KMN": list(ww.wgrad),
-                           "see": "the headline step"},
+                           "see": "the headline step", "standalone": wg_alone},
         }
         out["configs"]["qwen2_7b_plan"], plan_sample = codec_config(args, hl, wl, "qwen2_7b_plan")
         stress, stress_sample = codec_config(args, hl, wl, "llama3_8b_stress")
